@@ -1,0 +1,121 @@
+"""Pins of the oracle's Philox generator, sampler, reward hash and GRPO
+advantages against published values, distributions and closed forms."""
+import math
+
+import numpy as np
+import pytest
+from scipy import stats
+
+from oracle import grpo, reward, sampler
+from oracle.philox import philox4x32
+
+
+def test_philox_known_answers():
+    # published known-answer vectors of Philox4x32-10 (Random123 distribution)
+    f = 0xFFFFFFFF
+    cases = [((0, 0, 0, 0), (0, 0), (0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8)),
+             ((f, f, f, f), (f, f), (0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD)),
+             ((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344), (0xA4093822, 0x299F31D0),
+              (0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1))]
+    for ctr, key, want in cases:
+        got = tuple(int(x) for x in philox4x32(*ctr, *key))
+        assert got == want
+
+
+def test_uniforms_and_gumbel_moments():
+    u = np.concatenate([sampler.uniforms(99, 3, rid, pos, 4096) for rid in range(8) for pos in range(8)])
+    assert u.min() > 0 and u.max() < 1
+    assert abs(u.mean() - 0.5) < 5 * math.sqrt(1 / 12 / len(u))
+    assert stats.kstest(u, "uniform").pvalue > 1e-4
+    g = np.concatenate([sampler.gumbel(5, 0, rid, 0, 4096) for rid in range(16)]).astype(np.float64)
+    assert abs(g.mean() - np.euler_gamma) < 5 * (math.pi / math.sqrt(6)) / math.sqrt(len(g))
+
+
+def test_gumbel_max_is_softmax_sampling():
+    V = 16
+    logits = np.linspace(-2, 1.5, V).astype(np.float32)
+    for T in (1.0, 0.7):
+        n = 20000
+        toks = np.array([sampler.sample(logits, T, 123, 0, rid, 3)[0] for rid in range(n)])
+        p = np.exp(logits.astype(np.float64) / T)
+        p /= p.sum()
+        obs = np.bincount(toks, minlength=V)
+        chi = stats.chisquare(obs, p * n)
+        assert chi.pvalue > 1e-4
+
+
+def test_token_is_lowest_id_on_ties():
+    sc = np.array([0.5, 2.0, 2.0, 1.0], dtype=np.float32)
+    assert int(np.argmax(sc)) == 1
+    assert sampler.near_tie(sc)
+
+
+def test_forced_eos_frequency():
+    thr = (1 << 32) // 800
+    hits = sum(sampler.forced_eos(77, 0, rid, pos, thr) for rid in range(400) for pos in range(400))
+    n = 160000
+    assert abs(hits - n / 800) < 5 * math.sqrt(n / 800)
+    assert not sampler.forced_eos(77, 0, 1, 1, 0)
+
+
+def test_splitmix64_published_outputs():
+    # SplitMix64 seeded with 0 (state += golden gamma, then the finalizer)
+    gamma = 0x9E3779B97F4A7C15
+    assert reward.mix64(gamma) == 0xE220A8397B1DCDAF
+    assert reward.mix64(2 * gamma) == 0x6E789E6AA1B965F4
+
+
+def test_reward_hash_two_codings_agree():
+    g = np.random.default_rng(0)
+    for _ in range(50):
+        toks = g.integers(0, 151936, size=g.integers(1, 60))
+        seed, step, uid = int(g.integers(0, 2**63)), int(g.integers(0, 300)), int(g.integers(0, 256))
+        h = reward.hash_tokens(seed, step, uid, toks)
+        z = reward.mix64_np(np.uint64((seed ^ reward.SEED_R_XOR) & reward.MASK) ^ reward.mix64_np(
+            np.uint64((step << 32) + uid)))
+        for t in toks:
+            z = reward.mix64_np(z ^ np.uint64(int(t) + 1))
+        assert int(z) == h
+
+
+def test_reward_frequency_tracks_p():
+    g = np.random.default_rng(1)
+    for p in (0.0, 0.03, 0.5, 0.9, 1.0):
+        n = 4000
+        r = [reward.reward_of_hash(reward.hash_tokens(9, 0, u, g.integers(0, 512, 8)), p) for u in range(n)]
+        if p in (0.0, 1.0):
+            assert sum(r) == n * p
+        else:
+            assert abs(np.mean(r) - p) < 5 * math.sqrt(p * (1 - p) / n)
+
+
+def test_grpo_binary_closed_form_and_saturation():
+    eps = 1e-6
+    offs = [0, 8, 16, 24, 28]
+    r = [1, 0, 0, 0, 0, 0, 0, 0] + [1] * 8 + [0] * 8 + [1, 1, 0, 1]
+    a = grpo.advantages(r, offs, eps)
+    for g in range(4):
+        lo, hi = offs[g], offs[g + 1]
+        m, s = hi - lo, sum(r[lo:hi])
+        if s in (0, m):
+            assert np.all(a[lo:hi] == 0.0)   # saturated group: zero advantage
+        else:
+            sd = math.sqrt(s * (m - s) / (m * (m - 1)))
+            for i in range(lo, hi):
+                want = ((1 - s / m) if r[i] else (-s / m)) / (sd + eps)
+                assert a[i] == pytest.approx(want, rel=1e-12)
+            assert abs(a[lo:hi].sum()) < 1e-12
+            assert a[lo:hi].std(ddof=1) == pytest.approx(sd / (sd + eps), rel=1e-9)
+
+
+def test_grpo_matches_library_statistics():
+    g = np.random.default_rng(3)
+    r = g.random(50)
+    offs = [0, 3, 10, 11, 30, 50]
+    a = grpo.advantages(r, offs)
+    for lo, hi in zip(offs, offs[1:]):
+        x = r[lo:hi]
+        if hi - lo >= 2:
+            assert np.allclose(a[lo:hi], (x - x.mean()) / (x.std(ddof=1) + 1e-6))
+        else:
+            assert np.all(a[lo:hi] == 0)
