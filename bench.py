@@ -1,0 +1,212 @@
+"""Benchmark of the SARA rollout-allocation hot path on one MI355X.
+
+One bench step = one allocation step of the named workload: prefill of the
+step's prompt pool, the decode / decide / refill loop until no prompt is
+active (replayed from a HIP graph), and GRPO advantages of the committed
+groups.  Inputs (weights, prompt pools) are resident in HBM before the timed
+region.  Prints one JSON line.
+
+value  = rollout tokens generated per second over the K timed steps.
+roofline: per-kernel HIP-event timing of one further allocation step run
+eagerly (every `--profile-every`-th decode step profiled); the dominant
+kernel is the class with the largest share of decode time, its achieved
+GB/s is algorithmic bytes / event-timed duration.
+cpu_baseline: the CPU oracle generating rollouts of the same model shape on a
+bounded sample (one prompt's prefill + a few rollouts x a few tokens).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def describe(cfg):
+    m, a = cfg["model"], cfg["alloc"]
+    return (f"{cfg['name']}: {m['n_layers']}L d{m['d_model']} {m['n_heads']}Q/{m['n_kv_heads']}KV x{m['head_dim']} "
+            f"ffn{m['d_ffn']} V{m['vocab']} {m['dtype']}; B={a['B']} k={a['k']} n0={a['n0']} tau={a['tau_low']} "
+            f"N={a['budget_N']} slots={a['n_slots']} pool={a['pool_U']} prompts U{list(cfg['prompt_len'])} "
+            f"max_new={a['max_new']} mode={a['mode']}")
+
+
+def cpu_baseline(cfg, weights, seconds_target=15.0):
+    """Oracle rollout generation rate on a bounded sample, host cores."""
+    from oracle import run as ORUN
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [os.cpu_count()])
+    except Exception:
+        threads = os.cpu_count()
+    c = W.get_config(cfg["name"])
+    a = c["alloc"]
+    pool = W.make_pool(c, 10_000)
+    seed = W.sampling_seed(c)
+    src = ORUN.RolloutSource(c, weights, pool, seed)
+    t0 = time.time()
+    for name, _ in W.weight_specs(c["model"]):   # weight conversion outside the timing
+        src.dec.w(name)
+    t_setup = time.time() - t0
+    rollouts, new_tokens = 2, 4
+    a_max = a["max_new"]
+    src.a = dict(a, max_new=new_tokens)
+    t0 = time.time()
+    src._generate([(0, j) for j in range(rollouts)])
+    t_run = time.time() - t0
+    n_tok = sum(src.results[(0, j)]["length"] for j in range(rollouts))
+    P = int(pool["offsets"][1] - pool["offsets"][0])
+    src.a = dict(a, max_new=a_max)
+    return dict(value=n_tok / t_run, unit="tokens/s", cores=int(threads), kind="oracle",
+                sample=(f"{cfg['name']} shape: prefill of one {P}-token prompt + {rollouts} rollouts x "
+                        f"{new_tokens} tokens (generated tokens / wall time incl. prefill; weight cache "
+                        f"warm-up {t_setup:.1f}s excluded)"),
+                seconds=t_run)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="qwen1p5b_shape")
+    ap.add_argument("--graph-iters", type=int, default=16)
+    ap.add_argument("--profile-every", type=int, default=16)
+    ap.add_argument("--no-profile", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the allocation step is "
+              f"single-GPU by design (see DESIGN.md, 'More than one GPU').", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2607_26253_amd as sara
+    assert torch.cuda.is_available(), "bench.py needs a HIP device"
+    torch.cuda.set_device(0)
+    cfg = W.get_config(args.config)
+    t0 = time.time()
+    weights = W.make_weights(cfg)
+    t_w = time.time() - t0
+    print(f"[bench] {describe(cfg)}; weights generated in {t_w:.1f}s", file=sys.stderr, flush=True)
+    dw = sara.upload_weights(W.weight_specs(cfg["model"]), weights)
+    ctx = sara.Sara(cfg["model"], cfg["alloc"], W.sampling_seed(cfg), dw)
+    del dw
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    n_total = args.warmup + args.steps + (0 if args.no_profile else 1)
+    pools = []
+    for s in range(n_total):
+        p = W.make_pool(cfg, s)
+        d_tok = torch.from_numpy(p["tokens"]).cuda()
+        d_p = torch.from_numpy(p["p"]).cuda()
+        d_fl = torch.from_numpy(np.ascontiguousarray(p["forced_len"].reshape(-1))).cuda() \
+            if p["forced_len"] is not None else None
+        pools.append((p, d_tok, d_p, d_fl))
+    torch.cuda.synchronize()
+
+    def one_step(i):
+        p, d_tok, d_p, d_fl = pools[i]
+        ctx.sara_begin_step(d_tok, p["offsets"], d_p, d_fl, p["step"])
+        ctx.sara_run(None, graph_iters=args.graph_iters)
+        ctx.sara_finish_step(1e-6)
+        return ctx.sara_query()
+
+    for i in range(args.warmup):
+        st = one_step(i)
+        print(f"[bench] warmup step {i}: {st['tokens']} tokens, {st['decode_steps']} decode steps",
+              file=sys.stderr, flush=True)
+
+    torch.cuda.synchronize()
+    stats = []
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        stats.append(one_step(args.warmup + i))
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    for i, st in enumerate(stats):
+        print(f"[bench] step {i}: tokens {st['tokens']} rollouts {st['rollouts']} committed {st['committed']} "
+              f"abandoned {st['abandoned']} drawn {st['drawn']} decode steps {st['decode_steps']}",
+              file=sys.stderr, flush=True)
+    tokens = sum(s["tokens"] for s in stats)
+    committed = sum(s["committed"] for s in stats)
+    rollouts = sum(s["rollouts"] for s in stats)
+    decode_steps = sum(s["decode_steps"] for s in stats)
+
+    out = {
+        "metric": "rollout tokens/s + effective groups/s on 1 GPU; decode HBM GB/s % of peak",
+        "value": tokens / dt, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": 1e3 * dt / args.steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg["model"]["dtype"],
+        "data": "synthetic (random-init weights, seeded prompt pools and success rates)",
+        "config": {"workload": describe(cfg)},
+        "effective_groups_per_s": committed / dt,
+        "rollouts_per_effective_group": (rollouts / committed) if committed else None,
+        "tokens_per_effective_group": (tokens / committed) if committed else None,
+        "decode_steps_per_s": decode_steps / dt,
+    }
+
+    if not args.no_profile:
+        p, d_tok, d_p, d_fl = pools[-1]
+        ctx.sara_begin_step(d_tok, p["offsets"], d_p, d_fl, p["step"])
+        ctx.sara_reset_profile()
+        it, n_prof = 0, 0
+        tprof = time.perf_counter()
+        while True:
+            if it % 16 == 0 and ctx.sara_query()["done"]:
+                break
+            on = (it % args.profile_every) == 0
+            ctx.sara_set_profiling(on)
+            ctx.sara_decode_step(None, None, False)
+            n_prof += int(on)
+            ctx.sara_posterior_decide()
+            ctx.sara_refill()
+            it += 1
+        ctx.sara_set_profiling(False)
+        prof = ctx.sara_read_profile()
+        tprof = time.perf_counter() - tprof
+        dec = [k for k in prof if k["launches"] > 0]
+        tot_ms = sum(k["ms"] for k in dec)
+        tot_by = sum(k["bytes"] for k in dec)
+        dom = max(dec, key=lambda k: k["ms"])
+        per_launch_ms = dom["ms"] / dom["launches"]
+        per_launch_by = dom["bytes"] / dom["launches"]
+        ach = per_launch_by / (per_launch_ms * 1e-3) / 1e9
+        out["roofline"] = {
+            "kernel": dom["name"], "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": ach / HBM_PEAK_GBS, "traffic": None,
+            "avg_launch_us": per_launch_ms * 1e3, "alg_bytes_per_launch": per_launch_by,
+            "launches_timed": dom["launches"],
+            "tflops": dom["flops"] / (dom["ms"] * 1e-3) / 1e12 if dom["flops"] else None,
+        }
+        out["decode_profile"] = {
+            "decode_steps_profiled": n_prof, "decode_steps": it,
+            "kernel_time_ms": tot_ms, "alg_bytes": tot_by,
+            "decode_hbm_gbs": tot_by / (tot_ms * 1e-3) / 1e9,
+            "decode_hbm_frac": tot_by / (tot_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "classes": {k["name"]: {"launches": k["launches"], "ms": round(k["ms"], 3),
+                                    "GBps": round(k["bytes"] / (k["ms"] * 1e-3) / 1e9, 1) if k["ms"] else None}
+                        for k in dec},
+            "wall_s": tprof,
+        }
+        print(f"[bench] profiled {n_prof} of {it} decode steps; dominant {dom['name']}: {ach:.0f} GB/s; "
+              f"decode kernels {out['decode_profile']['decode_hbm_gbs']:.0f} GB/s", file=sys.stderr, flush=True)
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, weights)
+    ctx.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

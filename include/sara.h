@@ -1,0 +1,247 @@
+/*
+ * sara.h - C ABI of libsara: the rollout-generation hot path of SARA
+ * (Sequential Adaptive Rollout Allocation) on one MI355X (gfx950).
+ *
+ * One allocation step (Algorithm 1, section 3.3) is driven by the host as
+ *
+ *     sara_begin_step(...)                      prompt pool in, prefill, first draws
+ *     repeat: sara_decode_step -> sara_posterior_decide -> sara_refill
+ *             (or sara_run, which replays that triple from a HIP graph)
+ *     until the step is done (sara_query / sara_run report it)
+ *     sara_finish_step(...)                     GRPO advantages of committed groups
+ *
+ * All calls enqueue work on the context's stream and return at once unless
+ * stated otherwise.  Pointers prefixed d_ are device (HIP) memory, h_ host
+ * memory.  Sizes are element counts.  The context is not thread safe: use one
+ * context per host thread and stream.
+ *
+ * Errors: every int-returning call returns SARA_OK or a negative code and
+ * sets a thread-local message readable with sara_last_error().  Argument
+ * errors are detected synchronously (SARA_EINVAL) and enqueue nothing.
+ * Budget or prompt-pool exhaustion is not an error: the step ends with fewer
+ * than B committed groups.
+ */
+#ifndef SARA_H
+#define SARA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct sara_ctx sara_ctx;
+
+enum {
+  SARA_OK = 0,
+  SARA_EINVAL = -1,   /* invalid argument or unsupported configuration         */
+  SARA_ENOMEM = -2,   /* device allocation failed                              */
+  SARA_EHIP = -3,     /* a HIP runtime call failed                             */
+  SARA_ESTATE = -4,   /* call out of order (e.g. decode before begin_step)     */
+  SARA_EDEVICE = -5   /* a device-side check failed (see sara_step_stats.error) */
+};
+enum { SARA_F32 = 0, SARA_BF16 = 1 };
+enum { SARA_MODE_SARA = 0, SARA_MODE_FIXED_K = 1 };
+/* decision codes in the decision log */
+enum { SARA_COMMIT = 1, SARA_ABANDON = 2, SARA_CONTINUE = 3 };
+/* per-prompt status */
+enum { SARA_UNDRAWN = 0, SARA_ACTIVE = 1, SARA_COMMITTED = 2, SARA_ABANDONED = 3 };
+
+/* Decoder shape.  Pre-norm GQA decoder: RMSNorm, rotate-half RoPE, SwiGLU,
+ * untied LM head, no biases.  head_dim in {64, 128}; n_heads a multiple of
+ * n_kv_heads with at most 8 query heads per KV head; d_model, d_ffn and
+ * n_heads*head_dim multiples of 32.  dtype SARA_BF16 stores weights, KV cache
+ * and GEMM inputs in bf16 (fp32 accumulation); SARA_F32 computes in fp32.
+ * eos_id = -1 disables the EOS token. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, d_ffn, vocab;
+  float rope_theta, rms_eps;
+  int32_t dtype;
+  int32_t eos_id;
+} sara_model_desc;
+
+/* Allocation problem of one step (Algorithm 1 inputs; implementation-details
+ * appendix for commit_min, the prior and the budget cap):
+ *   B           effective groups wanted (ignored in SARA_MODE_FIXED_K)
+ *   k           group size;  n0 probe rollouts per fresh prompt (1..k)
+ *   commit_min  commit floor (2..k); tau_low abandon threshold in [0, 1]
+ *   alpha0/beta0  Beta prior (> 0);  budget_N  rollout budget of the step
+ *   pool_U      prompts in the step's pool;  n_slots concurrent rollout slots
+ *   kv_block    KV page size in tokens (must be 16)
+ *   max_prompt  longest prompt;  max_new  generated-token cap per rollout
+ *   temperature sampling temperature (> 0);  top_p must be 1 (full softmax)
+ *   forced_eos_u32  per-token probability x / 2^32 of a forced EOS (0 = off)
+ *   prio_quant_bits  quantisation of the p_eff priority key (1..21)
+ *   seed        key material of the counter-based sampler and reward hash
+ * Limits: min(budget_N, pool_U * k) <= 4096 queued rollouts; pool_U < 2^26;
+ * n_slots <= 4096. */
+typedef struct {
+  int32_t B, k, n0, commit_min;
+  double tau_low, alpha0, beta0;
+  int64_t budget_N;
+  int32_t pool_U, n_slots, kv_block, max_prompt, max_new, mode;
+  float temperature, top_p;
+  uint32_t forced_eos_u32;
+  int32_t prio_quant_bits;
+  uint64_t seed;
+} sara_alloc_desc;
+
+typedef struct {
+  int32_t done;          /* 1 once no prompt is active                      */
+  int32_t error;         /* device error word, 0 = none                      */
+  int32_t decode_steps;  /* decode steps executed in this allocation step    */
+  int32_t drawn;         /* prompts drawn from the pool                      */
+  int32_t committed;     /* |C|: effective groups collected                  */
+  int32_t abandoned;
+  int32_t active;        /* |A|                                             */
+  int32_t queued;        /* rollouts waiting for a slot                      */
+  int32_t running;       /* occupied slots                                   */
+  int32_t pad_;
+  int64_t budget_left;   /* N - rollouts issued (k reserved per active prompt) */
+  int64_t rollouts;      /* rollouts issued                                  */
+  int64_t tokens;        /* tokens generated                                 */
+  int64_t n_decisions, n_draws, n_assigns, n_finishes;  /* log lengths       */
+} sara_step_stats;
+
+/* Create a context on the current HIP device.
+ * d_weights: n_weights device pointers in this order, each row-major
+ * [out][in] in the model dtype (bf16 as raw 16-bit patterns):
+ *   embed[V][d]; per layer l: attn_norm[d], wq[Hq*hd][d], wk[Hkv*hd][d],
+ *   wv[Hkv*hd][d], wo[d][Hq*hd], ffn_norm[d], wg[ffn][d], wu[ffn][d],
+ *   wd[d][ffn]; then final_norm[d], lm_head[V][d].
+ * n_weights must be 3 + 9 * n_layers.  The weights are copied (repacked)
+ * into library-owned memory; the caller may free its copies once the stream
+ * has passed this call.  stream: a hipStream_t, or NULL for the null stream.
+ * All KV, slot, controller and workspace memory is allocated here. */
+int sara_init(const sara_model_desc* model, const sara_alloc_desc* alloc,
+              const void* const* d_weights, int32_t n_weights, void* stream,
+              sara_ctx** out);
+
+/* Start an allocation step over a pool of pool_U prompts.
+ * d_tokens: concatenated prompt token ids (device, int32);
+ * h_offsets: pool_U + 1 host offsets into d_tokens (prompt u is
+ *   [h_offsets[u], h_offsets[u+1]), length 1..max_prompt);
+ * d_p: per-prompt success probability of the synthetic verifier (device, fp64);
+ * d_forced_len: NULL or [pool_U * k] forced rollout lengths in 1..max_new
+ *   (the token at that index becomes EOS and the rollout ends);
+ * step_index: enters the sampler key and the reward hash.
+ * The inputs are copied; the caller may reuse them once the stream has
+ * passed this call.  Enqueues: state reset, prefill of every prompt of the
+ * pool into its shared paged KV blocks, the first draws and slot
+ * assignments. */
+int sara_begin_step(sara_ctx* ctx, const int32_t* d_tokens, const int32_t* h_offsets,
+                    const double* d_p, const int32_t* d_forced_len, int32_t step_index);
+
+/* One decode step over every occupied slot: embedding, n_layers decoder
+ * layers over the paged KV cache, LM head, Gumbel-max sampling keyed by
+ * (seed, step_index, rollout id uid*k + j, generated index), forced EOS,
+ * reward hash, termination.
+ * d_forced_tok: NULL or [pool_U * k][max_new] teacher-forcing table (device);
+ * the forced token is appended and rewarded, the sampled one is recorded.
+ * d_logits: NULL or [n_slots][vocab] fp32 (device); receives the logits of
+ * each occupied slot's row.  model_free != 0 skips the decoder: the forced
+ * table (required) supplies every token. */
+int sara_decode_step(sara_ctx* ctx, const int32_t* d_forced_tok, float* d_logits,
+                     int32_t model_free);
+
+/* Apply the finished rollouts of the last decode step to their prompts'
+ * (n, s) and decide every quiescent active prompt with Eq. decide:
+ * Beta(alpha0 + s, beta0 + n - s), p_eff by Proposition 1 (fp64 lgamma),
+ * commit / abandon (refund k - n) / continue (queue more rollouts). */
+int sara_posterior_decide(sara_ctx* ctx);
+
+/* Draw fresh prompts while |A| < B - |C|, budget_left >= k and the pool is
+ * not exhausted; order the pending rollouts by (quantised p_eff desc, uid,
+ * j) and assign them to free slots in ascending slot order. */
+int sara_refill(sara_ctx* ctx);
+
+/* Drive the step to completion: replays [decode, decide, refill] from a HIP
+ * graph of graph_iters iterations, polling the done flag asynchronously.
+ * Synchronises before returning.  d_forced_tok as in sara_decode_step.
+ * *iters_out receives the number of loop iterations enqueued. */
+int sara_run(sara_ctx* ctx, const int32_t* d_forced_tok, int32_t graph_iters,
+             int64_t max_iters, int64_t* iters_out);
+
+/* Synchronise the stream and report the step's counters. */
+int sara_query(sara_ctx* ctx, sara_step_stats* out);
+
+/* Build the CSR of committed groups (ascending uid, rollouts in j order) and
+ * compute their GRPO advantages with grpo_group_advantages.  Enqueued. */
+int sara_finish_step(sara_ctx* ctx, float eps);
+
+/* Copy results to host (synchronises).  Any pointer may be NULL.
+ *   h_tokens  [pool_U*k][max_new] int32 appended tokens (-1 past the end)
+ *   h_sampled [pool_U*k][max_new] int32 sampler choices
+ *   h_len     [pool_U*k] int32 rollout lengths (0 = never issued)
+ *   h_reward  [pool_U*k] int32 rewards
+ *   h_status, h_n, h_s [pool_U] int32; h_peff [pool_U] fp64 (last p_eff) */
+int sara_read_rollouts(sara_ctx* ctx, int32_t* h_tokens, int32_t* h_sampled, int32_t* h_len,
+                       int32_t* h_reward, int32_t* h_status, int32_t* h_n, int32_t* h_s,
+                       double* h_peff);
+
+/* Copy logs to host (synchronises).  Row formats (int64 each):
+ *   decisions: (t, uid, code, n, s, p_eff bits as int64)   [n_decisions][6]
+ *   draws:     (t_start, uid)                               [n_draws][2]
+ *   assigns:   (t_start, slot, uid, j)                      [n_assigns][4]
+ *   finishes:  (t, slot, uid, j, length, reward)            [n_finishes][6]
+ * cap_* are row capacities of the buffers; rows beyond a capacity are dropped. */
+int sara_read_logs(sara_ctx* ctx, int64_t* h_dec, int64_t cap_dec, int64_t* h_draw,
+                   int64_t cap_draw, int64_t* h_asg, int64_t cap_asg, int64_t* h_fin,
+                   int64_t cap_fin);
+
+/* GRPO data of the last sara_finish_step (synchronises).
+ * h_offsets [committed + 1], h_rewards / h_adv [offsets[committed]]. */
+int sara_read_advantages(sara_ctx* ctx, int32_t* h_offsets, float* h_rewards, float* h_adv,
+                         int32_t cap);
+
+/* Closed-form predictor of Proposition 1 (Eq. peff) for count prompts:
+ * d_out[i] = P(group of size k is mixed | d_n[i] observed, d_s[i] successes)
+ * under the prior Beta(alpha0, beta0), fp64 via lgamma.  Pure; enqueued on
+ * stream. */
+int sara_peff_batch(const int32_t* d_n, const int32_t* d_s, int32_t k, double alpha0,
+                    double beta0, int32_t count, double* d_out, void* stream);
+
+/* Group-relative advantages of Eq. grpo: for group g with rewards
+ * d_r[d_group_off[g] .. d_group_off[g+1]), A_i = (r_i - mean) / (std + eps),
+ * std unbiased (m - 1); groups of size < 2 get 0.  d_group_off has
+ * n_groups + 1 entries (device).  Enqueued on stream. */
+int grpo_group_advantages(const float* d_r, const int32_t* d_group_off, int32_t n_groups,
+                          float eps, float* d_adv, void* stream);
+
+/* Sampler alone, for parity on given logits: rows r < n_rows, logits
+ * d_logits[r][vocab] fp32, rollout ids d_rid[r], generated indices d_pos[r]
+ * -> d_tok[r] (Gumbel-max at temperature, forced EOS if eos_id >= 0 and
+ * forced_eos_u32 > 0).  Enqueued on stream. */
+int sara_sample_logits(const float* d_logits, int32_t n_rows, int32_t vocab,
+                       const int32_t* d_rid, const int32_t* d_pos, uint64_t seed,
+                       int32_t step_index, float temperature, int32_t eos_id,
+                       uint32_t forced_eos_u32, int32_t* d_tok, void* stream);
+
+/* Per-kernel timing of eager decode steps.  While enabled, every
+ * sara_decode_step call (not the graph replays of sara_run) records a HIP
+ * event pair around each kernel it launches on the context's stream, waits
+ * for them before returning, and adds to that kernel's class the elapsed
+ * time and the algorithmic HBM bytes and flops of the launch (weights,
+ * activations and the K/V pages the kernel must touch; workspace traffic
+ * of split-K partials is not algorithmic and is not counted). */
+typedef struct {
+  char name[40];
+  int64_t launches;
+  double ms;      /* summed event-timed kernel time */
+  double bytes;   /* algorithmic bytes of those launches */
+  double flops;   /* algorithmic flops of those launches */
+} sara_kernel_profile;
+
+int sara_set_profiling(sara_ctx* ctx, int32_t enable);   /* totals are kept */
+int sara_reset_profile(sara_ctx* ctx);                   /* zero the totals */
+/* Copy up to cap classes (in a fixed order) and their totals; *n_out receives
+ * the number of classes. */
+int sara_read_profile(sara_ctx* ctx, sara_kernel_profile* out, int32_t cap, int32_t* n_out);
+
+void sara_destroy(sara_ctx* ctx);
+const char* sara_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SARA_H */

@@ -39,9 +39,12 @@ def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
 
 
 class Decoder:
-    def __init__(self, model: dict, weights: dict):
+    def __init__(self, model: dict, weights: dict, gemm_acc: str = "f32"):
+        """gemm_acc: accumulation of bf16 GEMMs, "f32" (a bf16 engine's) or
+        "f64" (used only to measure the model's sensitivity to rounding order)."""
         self.m = model
         self.bf16 = model["dtype"] == "bf16"
+        self.gemm_acc = gemm_acc
         self.L = model["n_layers"]
         self.d = model["d_model"]
         self.hq, self.hkv, self.hd = model["n_heads"], model["n_kv_heads"], model["head_dim"]
@@ -68,8 +71,10 @@ class Decoder:
     def mm(self, x, name):
         """x @ W^T with W stored [out, in]."""
         W = self.w(name)
-        if self.bf16:
+        if self.bf16 and self.gemm_acc == "f32":
             return (np.asarray(x, dtype=np.float32) @ W.T).astype(np.float64)
+        if self.bf16:
+            return np.asarray(x, dtype=np.float64) @ W.astype(np.float64).T
         return x @ W.T
 
     def rmsnorm(self, h, name):

@@ -22,7 +22,7 @@ from .model import Decoder
 
 class RolloutSource:
     def __init__(self, cfg, weights, pool, seed, step=None, forced_tokens=None,
-                 keep_logits=None, model_free=False):
+                 keep_logits=None, model_free=False, gemm_acc="f32"):
         self.cfg = cfg
         self.m, self.a = cfg["model"], cfg["alloc"]
         self.pool = pool
@@ -31,7 +31,7 @@ class RolloutSource:
         self.forced_tokens = forced_tokens           # dict rid -> int array, or [U*k, max_new]
         self.keep_logits = keep_logits              # callable(uid, j, i) -> bool, or None
         self.model_free = model_free
-        self.dec = None if model_free else Decoder(self.m, weights)
+        self.dec = None if model_free else Decoder(self.m, weights, gemm_acc=gemm_acc)
         self.prefix = {}
         self.results = {}
         self.logits = {}
@@ -119,9 +119,10 @@ class RolloutSource:
                 reward=reward.reward_of_hash(h, float(self.pool["p"][r["u"]])), near_ties=r["ties"])
 
 
-def run_step(cfg, weights, pool, seed, forced_tokens=None, keep_logits=None, model_free=False):
+def run_step(cfg, weights, pool, seed, forced_tokens=None, keep_logits=None, model_free=False,
+             gemm_acc="f32"):
     src = RolloutSource(cfg, weights, pool, seed, forced_tokens=forced_tokens,
-                        keep_logits=keep_logits, model_free=model_free)
+                        keep_logits=keep_logits, model_free=model_free, gemm_acc=gemm_acc)
     res = controller.simulate(cfg["alloc"], len(pool["p"]), src.outcomes)
     k = cfg["alloc"]["k"]
     offs, rws = [0], []

@@ -1,0 +1,836 @@
+// Decoder kernels of the rollout decode step and the prompt prefill (gfx950).
+//
+// Per layer, over the rows of a batch (occupied slots in decode, prompt
+// tokens in prefill):
+//   gemm(x, W_qkv) -> qkv epilogue (split-K sum, RoPE, bf16 q, paged KV append)
+//   paged GQA attention over ragged contexts (split-context + combine)
+//   gemm(o, W_o)   -> residual add + RMSNorm -> x
+//   gemm(x, W_gu)  -> SwiGLU -> a
+//   gemm(a, W_d)   -> residual add + RMSNorm of the next layer (or final) -> x
+// then the LM head gemm and the Gumbel-max sampler.
+//
+// GEMMs take both operands with K contiguous ([rows][K]) and run on the
+// bf16 MFMA (v_mfma_f32_16x16x32_bf16) with fp32 accumulation; split-K
+// partials go to a workspace and are summed in split order by the epilogue,
+// so results do not depend on scheduling.  The fp32 model uses a VALU GEMM.
+#include "sara_internal.h"
+
+#include <math.h>
+
+namespace sara {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// block reductions (fixed tree order -> deterministic)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+// sum over a 256-thread block; every thread gets the result
+__device__ float block_sum256(float v, float* red) {
+  v = wave_sum(v);
+  int w = threadIdx.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  float r = (red[0] + red[1]) + (red[2] + red[3]);
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// embedding gather + first RMSNorm (decode and prefill rows)
+// ---------------------------------------------------------------------------
+// Decode rows: row i of the batch is occupied slot active[i].
+__global__ __launch_bounds__(256) void k_decode_rows(const Ctl* __restrict__ ctl,
+    const int32_t* __restrict__ active, const int32_t* __restrict__ slot_uid,
+    const int32_t* __restrict__ slot_j, const int32_t* __restrict__ slot_gen,
+    const int32_t* __restrict__ tok, const int32_t* __restrict__ off,
+    const int32_t* __restrict__ out_tok, int k, int max_new, RowDesc* __restrict__ rows) {
+  int M = ctl->done ? 0 : ctl->M;
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= M) return;
+  int s = active[i];
+  int u = slot_uid[s], j = slot_j[s], g = slot_gen[s];
+  int P = off[u + 1] - off[u];
+  int rid = u * k + j;
+  RowDesc r;
+  r.tok = (g == 0) ? tok[off[u] + P - 1] : out_tok[(size_t)rid * max_new + g - 1];
+  r.pos = P - 1 + g;
+  r.plen = P - 1;
+  r.tab = s;
+  r.slot = s;
+  r.rid = rid;
+  r.gen = g;
+  r.uid = u;
+  rows[i] = r;
+}
+
+// Prefill rows of the chunk [r0, r0 + n): global prompt-token row r maps to
+// prompt u (pre[u] <= r < pre[u+1]) and token t = r - pre[u].
+__global__ __launch_bounds__(256) void k_prefill_rows(const int32_t* __restrict__ pre, int U,
+    int r0, int n, const int32_t* __restrict__ tok, const int32_t* __restrict__ off, int S,
+    RowDesc* __restrict__ rows, int32_t* __restrict__ rows_M) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i == 0) *rows_M = n;
+  if (i >= n) return;
+  int r = r0 + i;
+  int lo = 0, hi = U;  // largest u with pre[u] <= r
+  while (hi - lo > 1) {
+    int mid = (lo + hi) >> 1;
+    if (pre[mid] <= r) lo = mid; else hi = mid;
+  }
+  int u = lo, t = r - pre[u];
+  RowDesc d;
+  d.tok = tok[off[u] + t];
+  d.pos = t;
+  d.plen = off[u + 1] - off[u] - 1;
+  d.tab = S + u;
+  d.slot = -1;
+  d.rid = -1;
+  d.gen = -1;
+  d.uid = u;
+  rows[i] = d;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_embed_norm(const int32_t* __restrict__ M_ptr,
+    const RowDesc* __restrict__ rows, const T* __restrict__ embed, const float* __restrict__ w,
+    int d, float eps, float* __restrict__ h, T* __restrict__ x) {
+  __shared__ float red[4];
+  int i = blockIdx.x;
+  if (i >= *M_ptr) return;
+  int t = rows[i].tok;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    float v = ld_f32(embed, (size_t)t * d + c);
+    h[(size_t)i * d + c] = v;
+    ss += v * v;
+  }
+  float tot = block_sum256(ss, red);
+  float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  for (int c = threadIdx.x; c < d; c += 256)
+    st_f32(x, (size_t)i * d + c, h[(size_t)i * d + c] * inv * w[c]);
+}
+
+// ---------------------------------------------------------------------------
+// GEMM: out[s][m][n] = sum_{k in split s} X[m][k] * W[n][k]
+// ---------------------------------------------------------------------------
+// bf16 MFMA.  A wave owns 16 weight rows (n) and MT tiles of 16 activation
+// rows (m).  Both operands are read straight from global memory in the MFMA
+// operand layout: lane l supplies row (l % 16) and the 8 consecutive k of
+// k-group (l / 16); the k-groups of the two operands coincide, so the
+// product is exact for any assignment of k to groups.  A 128-wide k step
+// loads 64 B per lane per row (256 B contiguous per row per wave).
+template <int MT>
+__global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ X,
+    const uint16_t* __restrict__ W, float* __restrict__ out, const int32_t* __restrict__ M_ptr,
+    int N, int K, int kps, int64_t split_stride) {
+  const int M = *M_ptr;
+  const int m_base = blockIdx.z * 16 * MT;
+  if (m_base >= M) return;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int n0 = (blockIdx.x * 4 + wave) * 16;
+  if (n0 >= N) return;
+  const int row = lane & 15, grp = lane >> 4;
+  const int k_begin = blockIdx.y * kps;
+  const int k_end = min(K, k_begin + kps);
+  const uint16_t* wrow = W + (size_t)(n0 + row) * K + 8 * grp;
+  const uint16_t* xrow[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    int m = min(m_base + 16 * t + row, M - 1);
+    xrow[t] = X + (size_t)m * K + 8 * grp;
+  }
+  f32x4 acc[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  int kk = k_begin;
+  for (; kk + 128 <= k_end; kk += 128) {
+    uint4 wv[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) wv[c] = *(const uint4*)(wrow + kk + 32 * c);
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      uint4 xv[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) xv[c] = *(const uint4*)(xrow[t] + kk + 32 * c);
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wv[c]),
+                                                         __builtin_bit_cast(bf16x8, xv[c]), acc[t], 0, 0, 0);
+    }
+  }
+  for (; kk < k_end; kk += 32) {
+    uint4 wv = *(const uint4*)(wrow + kk);
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      uint4 xv = *(const uint4*)(xrow[t] + kk);
+      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wv),
+                                                       __builtin_bit_cast(bf16x8, xv), acc[t], 0, 0, 0);
+    }
+  }
+  // D[i][j]: i = weight row 4*grp + r, j = activation row (lane % 16)
+  float* o = out + (size_t)blockIdx.y * split_stride;
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+    int m = m_base + 16 * t + row;
+    if (m < M) *(f32x4*)(o + (size_t)m * N + n0 + 4 * grp) = acc[t];
+  }
+}
+
+// fp32 VALU GEMM for the fp32 model: 16x16 output tile per 256-thread block.
+__global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X,
+    const float* __restrict__ W, float* __restrict__ out, const int32_t* __restrict__ M_ptr,
+    int N, int K, int kps, int64_t split_stride) {
+  __shared__ float xs[16][33];
+  __shared__ float wsm[16][33];
+  const int M = *M_ptr;
+  const int m0 = blockIdx.z * 16, n0 = blockIdx.x * 16;
+  if (m0 >= M) return;
+  const int ty = threadIdx.x >> 4, tx = threadIdx.x & 15;
+  const int k_begin = blockIdx.y * kps, k_end = min(K, k_begin + kps);
+  float acc = 0.f;
+  for (int kk = k_begin; kk < k_end; kk += 32) {
+    for (int e = threadIdx.x; e < 16 * 32; e += 256) {
+      int r = e >> 5, c = e & 31;
+      int m = min(m0 + r, M - 1), n = min(n0 + r, N - 1);
+      bool in = kk + c < k_end;
+      xs[r][c] = in ? X[(size_t)m * K + kk + c] : 0.f;
+      wsm[r][c] = in ? W[(size_t)n * K + kk + c] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < 32; ++c) acc = fmaf(xs[ty][c], wsm[tx][c], acc);
+    __syncthreads();
+  }
+  int m = m0 + ty, n = n0 + tx;
+  if (m < M && n < N) out[(size_t)blockIdx.y * split_stride + (size_t)m * N + n] = acc;
+}
+
+// ---------------------------------------------------------------------------
+// epilogues
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float split_sum(const float* ws, int splits, int64_t stride, size_t idx) {
+  float v = 0.f;
+  for (int s = 0; s < splits; ++s) v += ws[(size_t)s * stride + idx];
+  return v;
+}
+
+// Page of position pos: block-table entries [0, PB) map the shared prompt
+// segment (positions < plen), entries [PB, MAXB) the private segment that
+// starts at position plen.
+__device__ __forceinline__ size_t kv_index(const RowDesc& r, const int32_t* btab, int MAXB, int PB,
+                                           int layer, int64_t n_blocks, int hkv, int g, int hd,
+                                           int dim, int pos) {
+  int e, o;
+  if (pos < r.plen) { e = pos >> 4; o = pos & 15; }
+  else { int q = pos - r.plen; e = PB + (q >> 4); o = q & 15; }
+  int64_t b = btab[(size_t)r.tab * MAXB + e];
+  return ((((size_t)layer * n_blocks + b) * hkv + g) * kBlockTok + o) * hd + dim;
+}
+
+// Split-K sum of the fused q|k|v output, rotate-half RoPE on q and k,
+// q -> bf16 buffer, k and v -> the row's KV page.
+template <typename T>
+__global__ __launch_bounds__(256) void k_qkv_epilogue(const int32_t* __restrict__ M_ptr,
+    const RowDesc* __restrict__ rows, const float* __restrict__ ws, int splits, int64_t stride,
+    const float2* __restrict__ rope, int hq, int hkv, int hd, int layer, int64_t n_blocks,
+    const int32_t* __restrict__ btab, int MAXB, int PB, T* __restrict__ qbuf, T* __restrict__ kc,
+    T* __restrict__ vc) {
+  int i = blockIdx.x;
+  if (i >= *M_ptr) return;
+  const RowDesc r = rows[i];
+  const int half = hd >> 1, nh = hq + 2 * hkv, N = nh * hd;
+  for (int e = threadIdx.x; e < nh * half; e += 256) {
+    int h = e / half, c = e - h * half;
+    size_t base = (size_t)i * N + (size_t)h * hd;
+    float a = split_sum(ws, splits, stride, base + c);
+    float b = split_sum(ws, splits, stride, base + c + half);
+    if (h < hq + hkv) {
+      float2 cs = rope[(size_t)r.pos * half + c];
+      float ra = a * cs.x - b * cs.y;
+      float rb = b * cs.x + a * cs.y;
+      if (h < hq) {
+        size_t q = ((size_t)i * hq + h) * hd;
+        st_f32(qbuf, q + c, ra);
+        st_f32(qbuf, q + c + half, rb);
+      } else {
+        int g = h - hq;
+        st_f32(kc, kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, hd, c, r.pos), ra);
+        st_f32(kc, kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, hd, c + half, r.pos), rb);
+      }
+    } else {
+      int g = h - hq - hkv;
+      st_f32(vc, kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, hd, c, r.pos), a);
+      st_f32(vc, kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, hd, c + half, r.pos), b);
+    }
+  }
+}
+
+// h += split-K sum; x = RMSNorm(h) * w  (stored in the model dtype)
+template <typename T>
+__global__ __launch_bounds__(256) void k_residual_norm(const int32_t* __restrict__ M_ptr,
+    const float* __restrict__ ws, int splits, int64_t stride, int d, float* __restrict__ h,
+    const float* __restrict__ w, float eps, T* __restrict__ x) {
+  __shared__ float red[4];
+  int i = blockIdx.x;
+  if (i >= *M_ptr) return;
+  float ss = 0.f;
+  for (int c = threadIdx.x; c < d; c += 256) {
+    size_t idx = (size_t)i * d + c;
+    float v = h[idx] + split_sum(ws, splits, stride, idx);
+    h[idx] = v;
+    ss += v * v;
+  }
+  float tot = block_sum256(ss, red);
+  float inv = 1.0f / sqrtf(tot / (float)d + eps);
+  for (int c = threadIdx.x; c < d; c += 256) {
+    size_t idx = (size_t)i * d + c;
+    st_f32(x, idx, h[idx] * inv * w[c]);
+  }
+}
+
+// a = silu(g) * u from the fused gate|up output ([m][2*ffn])
+template <typename T>
+__global__ __launch_bounds__(256) void k_swiglu(const int32_t* __restrict__ M_ptr,
+    const float* __restrict__ ws, int splits, int64_t stride, int ffn, T* __restrict__ a) {
+  int i = blockIdx.y;
+  if (i >= *M_ptr) return;
+  int f = blockIdx.x * 256 + threadIdx.x;
+  if (f >= ffn) return;
+  size_t base = (size_t)i * 2 * ffn;
+  float g = split_sum(ws, splits, stride, base + f);
+  float u = split_sum(ws, splits, stride, base + ffn + f);
+  float sg = g / (1.0f + expf(-g));
+  st_f32(a, (size_t)i * ffn + f, sg * u);
+}
+
+// ---------------------------------------------------------------------------
+// paged GQA attention
+// ---------------------------------------------------------------------------
+// Block (row i, KV head g, context split c) attends the G query heads of KV
+// head g over positions [c*SPLIT, min(ctx, (c+1)*SPLIT)) of the row's
+// sequence with an online softmax, tiles of 64 tokens staged in LDS; the
+// unnormalised output, running max and sum go to a partial buffer that the
+// combine kernel merges across splits.  Pages come from the block table:
+// positions below plen live in the prompt's shared pages, later ones in the
+// row's private pages.
+template <typename T, int HD>
+__global__ __launch_bounds__(256) void k_attention(const int32_t* __restrict__ M_ptr,
+    const RowDesc* __restrict__ rows, const T* __restrict__ qbuf, const T* __restrict__ kc,
+    const T* __restrict__ vc, const int32_t* __restrict__ btab, int MAXB, int PB, int layer,
+    int64_t n_blocks, int hq, int hkv, int n_splits, float scale, float* __restrict__ part) {
+  __shared__ float q_s[kMaxGroup][HD];
+  __shared__ float k_s[kAttnTile][HD + 1];
+  __shared__ float v_s[kAttnTile][HD];
+  __shared__ float p_s[kMaxGroup][kAttnTile];
+  __shared__ float m_s[kMaxGroup], l_s[kMaxGroup], al_s[kMaxGroup];
+  const int i = blockIdx.x, g = blockIdx.y, c = blockIdx.z;
+  if (i >= *M_ptr) return;
+  const RowDesc r = rows[i];
+  const int ctx = r.pos + 1;
+  const int t0 = c * kAttnSplit;
+  if (t0 >= ctx) return;
+  const int t1 = min(ctx, t0 + kAttnSplit);
+  const int G = hq / hkv;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  constexpr int DPT = HD / 64;  // dims per thread in the PV product
+  for (int e = tid; e < G * HD; e += 256) {
+    int gh = e / HD, dd = e - gh * HD;
+    q_s[gh][dd] = ld_f32(qbuf, ((size_t)i * hq + g * G + gh) * HD + dd);
+  }
+  if (tid < kMaxGroup) { m_s[tid] = -INFINITY; l_s[tid] = 0.f; }
+  float o[2][DPT];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < DPT; ++b) o[a][b] = 0.f;
+  __syncthreads();
+  for (int ts = t0; ts < t1; ts += kAttnTile) {
+    const int n = min(kAttnTile, t1 - ts);
+    for (int e = tid; e < n * HD; e += 256) {
+      int tk = e / HD, dd = e - tk * HD;
+      size_t idx = kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, dd, ts + tk);
+      k_s[tk][dd] = ld_f32(kc, idx);
+      v_s[tk][dd] = ld_f32(vc, idx);
+    }
+    __syncthreads();
+    // scores: thread (token lane, head wave / wave + 4)
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      int gh = wave + 4 * a;
+      if (gh < G) {
+        float sc = -INFINITY;
+        if (lane < n) {
+          float acc = 0.f;
+#pragma unroll 8
+          for (int dd = 0; dd < HD; ++dd) acc = fmaf(q_s[gh][dd], k_s[lane][dd], acc);
+          sc = acc * scale;
+        }
+        p_s[gh][lane] = sc;
+      }
+    }
+    __syncthreads();
+    // online softmax update, one wave per head pair
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      int gh = wave + 4 * a;
+      if (gh < G) {
+        float sc = p_s[gh][lane];
+        float mt = wave_max(sc);
+        float mo = m_s[gh];
+        float mn = fmaxf(mo, mt);
+        float pv = (lane < n) ? expf(sc - mn) : 0.f;
+        float sum = wave_sum(pv);
+        p_s[gh][lane] = pv;
+        if (lane == 0) {
+          float al = expf(mo - mn);
+          al_s[gh] = al;
+          l_s[gh] = l_s[gh] * al + sum;
+          m_s[gh] = mn;
+        }
+      }
+    }
+    __syncthreads();
+    // o = o * alpha + P V ; thread (dims lane*DPT.., heads wave, wave + 4)
+#pragma unroll
+    for (int a = 0; a < 2; ++a) {
+      int gh = wave + 4 * a;
+      if (gh < G) {
+        float al = al_s[gh];
+#pragma unroll
+        for (int b = 0; b < DPT; ++b) o[a][b] *= al;
+        for (int tk = 0; tk < n; ++tk) {
+          float pv = p_s[gh][tk];
+#pragma unroll
+          for (int b = 0; b < DPT; ++b) o[a][b] = fmaf(pv, v_s[tk][lane * DPT + b], o[a][b]);
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // partial layout: [row][g][split][gh][HD + 2]  (o..., m, l)
+#pragma unroll
+  for (int a = 0; a < 2; ++a) {
+    int gh = wave + 4 * a;
+    if (gh < G) {
+      float* dst = part + ((((size_t)i * hkv + g) * n_splits + c) * kMaxGroup + gh) * (HD + 2);
+#pragma unroll
+      for (int b = 0; b < DPT; ++b) dst[lane * DPT + b] = o[a][b];
+      if (lane == 0) { dst[HD] = m_s[gh]; dst[HD + 1] = l_s[gh]; }
+    }
+  }
+}
+
+// merge the context splits of every (row, query head) into o (model dtype)
+template <typename T, int HD>
+__global__ __launch_bounds__(HD) void k_attn_combine(const int32_t* __restrict__ M_ptr,
+    const RowDesc* __restrict__ rows, const float* __restrict__ part, int hq, int hkv,
+    int n_splits, T* __restrict__ out) {
+  int i = blockIdx.x, h = blockIdx.y;
+  if (i >= *M_ptr) return;
+  int G = hq / hkv, g = h / G, gh = h - g * G;
+  int ctx = rows[i].pos + 1;
+  int ns = (ctx + kAttnSplit - 1) / kAttnSplit;
+  const float* base = part + (((size_t)i * hkv + g) * n_splits * kMaxGroup + gh) * (HD + 2);
+  const size_t sstride = (size_t)kMaxGroup * (HD + 2);
+  float mx = -INFINITY;
+  for (int c = 0; c < ns; ++c) mx = fmaxf(mx, base[c * sstride + HD]);
+  float num = 0.f, den = 0.f;
+  for (int c = 0; c < ns; ++c) {
+    const float* p = base + c * sstride;
+    float wgt = expf(p[HD] - mx);
+    num += wgt * p[threadIdx.x];
+    den += wgt * p[HD + 1];
+  }
+  st_f32(out, ((size_t)i * hq + h) * HD + threadIdx.x, num / den);
+}
+
+// ---------------------------------------------------------------------------
+// sampler: Gumbel-max over the vocabulary with Philox4x32-10 noise
+// ---------------------------------------------------------------------------
+// score_v = fp32(logit_v / T) + fp32(-log(-log u_v)), u_v from word v % 4 of
+// Philox(rid, gen, v / 4, 0); the token is the lowest id of the max score.
+__device__ __forceinline__ void better(float& bs, int& bi, float s, int i) {
+  if (s > bs || (s == bs && i < bi)) { bs = s; bi = i; }
+}
+
+__global__ __launch_bounds__(256) void k_sample_partial(const int32_t* __restrict__ M_ptr,
+    const int32_t* __restrict__ rid_arr, const int32_t* __restrict__ pos_arr,
+    const RowDesc* __restrict__ rows, const float* __restrict__ logits, int V,
+    const CtlParams* __restrict__ cpd, uint64_t seed, int32_t step, float temp,
+    float* __restrict__ best, int32_t* __restrict__ bidx) {
+  __shared__ float sb[256];
+  __shared__ int si[256];
+  const int i = blockIdx.x, c = blockIdx.y;
+  if (i >= *M_ptr) return;
+  const int rid = rows ? rows[i].rid : rid_arr[i];
+  const int gen = rows ? rows[i].gen : pos_arr[i];
+  if (cpd) { seed = cpd->seed; step = cpd->step; temp = cpd->temperature; }
+  uint32_t k0, k1;
+  sampler_key(seed, step, k0, k1);
+  const int nblk = (V + 3) >> 2;
+  const int per = (nblk + kSampleChunks - 1) / kSampleChunks;
+  const int b0 = c * per, b1 = min(nblk, b0 + per);
+  const float* lg = logits + (size_t)i * V;
+  float bs = -INFINITY;
+  int bi = 0x7FFFFFFF;
+  for (int b = b0 + threadIdx.x; b < b1; b += 256) {
+    U32x4 w = philox4x32_10((uint32_t)rid, (uint32_t)gen, (uint32_t)b, 0u, k0, k1);
+    uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      int v = 4 * b + e;
+      if (v < V) {
+        double u = ((double)(ws[e] >> 8) + 0.5) * 0x1p-24;
+        float gmb = (float)(-log(-log(u)));
+        float s = __fadd_rn(__fdiv_rn(lg[v], temp), gmb);
+        better(bs, bi, s, v);
+      }
+    }
+  }
+  sb[threadIdx.x] = bs;
+  si[threadIdx.x] = bi;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (threadIdx.x < o) {
+      float s2 = sb[threadIdx.x + o];
+      int i2 = si[threadIdx.x + o];
+      if (s2 > sb[threadIdx.x] || (s2 == sb[threadIdx.x] && i2 < si[threadIdx.x])) {
+        sb[threadIdx.x] = s2;
+        si[threadIdx.x] = i2;
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    best[(size_t)i * kSampleChunks + c] = sb[0];
+    bidx[(size_t)i * kSampleChunks + c] = si[0];
+  }
+}
+
+__device__ __forceinline__ int reduce_chunks(const float* best, const int32_t* bidx, int i) {
+  float bs = -INFINITY;
+  int bi = 0x7FFFFFFF;
+  for (int c = 0; c < kSampleChunks; ++c)
+    better(bs, bi, best[(size_t)i * kSampleChunks + c], bidx[(size_t)i * kSampleChunks + c]);
+  return bi;
+}
+
+__device__ __forceinline__ bool forced_eos_fires(uint64_t seed, int32_t step, int rid, int gen,
+                                                 uint32_t thr) {
+  if (thr == 0u) return false;
+  uint32_t k0, k1;
+  sampler_key(seed, step, k0, k1);
+  U32x4 w = philox4x32_10((uint32_t)rid, (uint32_t)gen, 0u, 1u, k0, k1);
+  return w.x < thr;
+}
+
+// Final token of each decode row: forced EOS, teacher forcing, forced length,
+// reward hash chain, termination and the per-slot finish flag.
+__global__ __launch_bounds__(256) void k_sample_final(const Ctl* __restrict__ ctl,
+    const RowDesc* __restrict__ rows, const float* __restrict__ best,
+    const int32_t* __restrict__ bidx, const int32_t* __restrict__ forced,
+    const int32_t* __restrict__ flen, int model_free, const CtlParams* __restrict__ cpp,
+    const double* __restrict__ p, int32_t* __restrict__ out_tok, int32_t* __restrict__ samp_tok,
+    int32_t* __restrict__ slot_gen, uint64_t* __restrict__ slot_hash, int32_t* __restrict__ fin,
+    int32_t* __restrict__ r_len, int32_t* __restrict__ r_reward) {
+  int M = ctl->done ? 0 : ctl->M;
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= M) return;
+  const CtlParams cp = *cpp;
+  if (!cp.has_flen) flen = nullptr;
+  const RowDesc r = rows[i];
+  const int rid = r.rid, gen = r.gen, s = r.slot;
+  int samp;
+  if (model_free) {
+    samp = forced[(size_t)rid * cp.max_new + gen];
+  } else {
+    samp = reduce_chunks(best, bidx, i);
+    if (cp.eos >= 0 && forced_eos_fires(cp.seed, cp.step, rid, gen, cp.forced_eos)) samp = cp.eos;
+  }
+  int tok = forced ? forced[(size_t)rid * cp.max_new + gen] : samp;
+  bool done = false;
+  if (flen && gen + 1 == flen[rid]) {
+    if (cp.eos >= 0) tok = cp.eos;
+    done = true;
+  }
+  if (cp.eos >= 0 && tok == cp.eos) done = true;
+  if (gen + 1 == cp.max_new) done = true;
+  out_tok[(size_t)rid * cp.max_new + gen] = tok;
+  samp_tok[(size_t)rid * cp.max_new + gen] = samp;
+  uint64_t hsh = mix64(slot_hash[s] ^ (uint64_t)(uint32_t)(tok + 1));
+  slot_hash[s] = hsh;
+  slot_gen[s] = gen + 1;
+  if (done) {
+    r_len[rid] = gen + 1;
+    double u = (double)(hsh >> 11) * 0x1p-53;
+    r_reward[rid] = (u < p[r.uid]) ? 1 : 0;
+    fin[s] = 1;
+  }
+}
+
+// stand-alone sampler for given logits (parity entry point)
+__global__ void k_sample_rows_final(int n_rows, const int32_t* __restrict__ rid,
+    const int32_t* __restrict__ pos, const float* __restrict__ best,
+    const int32_t* __restrict__ bidx, uint64_t seed, int32_t step, int eos, uint32_t feos,
+    int32_t* __restrict__ tok) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n_rows) return;
+  int t = reduce_chunks(best, bidx, i);
+  if (eos >= 0 && forced_eos_fires(seed, step, rid[i], pos[i], feos)) t = eos;
+  tok[i] = t;
+}
+
+__global__ void k_copy_logits(const Ctl* __restrict__ ctl, const RowDesc* __restrict__ rows,
+                              const float* __restrict__ ws, int V, float* __restrict__ dst) {
+  int M = ctl->done ? 0 : ctl->M;
+  int i = blockIdx.y;
+  if (i >= M) return;
+  int s = rows[i].slot;
+  for (int v = blockIdx.x * 256 + threadIdx.x; v < V; v += gridDim.x * 256)
+    dst[(size_t)s * V + v] = ws[(size_t)i * V + v];
+}
+
+// M of the decode batch as a plain device int for the shared kernels
+__global__ void k_decode_M(const Ctl* __restrict__ ctl, int32_t* __restrict__ M_out) {
+  *M_out = ctl->done ? 0 : ctl->M;
+}
+
+// ---------------------------------------------------------------------------
+// host launchers
+// ---------------------------------------------------------------------------
+static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr, int M_cap,
+                int N, int K, int& splits_out, int max_splits = 1 << 30) {
+  int64_t stride = (int64_t)M_cap * N;
+  if (c->md.dtype == SARA_BF16) {
+    constexpr int MT = 8;
+    int tiles_n = (N + 63) / 64;
+    int zb = (M_cap + 16 * MT - 1) / (16 * MT);
+    int want = (tiles_n * zb >= 512) ? 1 : (512 + tiles_n * zb - 1) / (tiles_n * zb);
+    int chunks = K / 32;
+    int splits = want < chunks ? want : chunks;
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    int kps = ((chunks + splits - 1) / splits) * 32;
+    splits = (K + kps - 1) / kps;
+    if ((int64_t)splits * stride > c->ws_floats) { splits = 1; kps = K; }
+    dim3 grid(tiles_n, splits, zb);
+    hipLaunchKernelGGL(k_gemm_bf16<MT>, grid, dim3(256), 0, c->stream, (const uint16_t*)X,
+                       (const uint16_t*)W, c->ws, M_ptr, N, K, kps, stride);
+    splits_out = splits;
+  } else {
+    int tiles_n = (N + 15) / 16, zb = (M_cap + 15) / 16;
+    int want = (tiles_n * zb >= 256) ? 1 : (256 + tiles_n * zb - 1) / (tiles_n * zb);
+    int chunks = K / 32;
+    int splits = want < chunks ? want : chunks;
+    if (splits > max_splits) splits = max_splits;
+    if (splits < 1) splits = 1;
+    int kps = ((chunks + splits - 1) / splits) * 32;
+    splits = (K + kps - 1) / kps;
+    if ((int64_t)splits * stride > c->ws_floats) { splits = 1; kps = K; }
+    dim3 grid(tiles_n, splits, zb);
+    hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, c->stream, (const float*)X, (const float*)W,
+                       c->ws, M_ptr, N, K, kps, stride);
+    splits_out = splits;
+  }
+  return SARA_OK;
+}
+
+#define PROF_B(c) do { if ((c)->prof_active) prof_begin(c); } while (0)
+#define PROF_E(c, cls, N, K) do { if ((c)->prof_active) prof_end((c), (cls), (N), (K)); } while (0)
+
+template <typename T, int HD>
+static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_norm_out) {
+  hipStream_t st = c->stream;
+  const int d = c->d;
+  const int64_t stride_qkv = (int64_t)M_cap * c->nqkv;
+  T* x = (T*)c->x;
+  for (int l = 0; l < c->L; ++l) {
+    int sp;
+    PROF_B(c);
+    gemm(c, x, c->w_qkv[l], M_ptr, M_cap, c->nqkv, d, sp);
+    PROF_E(c, kPGemm, c->nqkv, d);
+    PROF_B(c);
+    hipLaunchKernelGGL(k_qkv_epilogue<T>, dim3(M_cap), dim3(256), 0, st, M_ptr, c->rows, c->ws, sp,
+                       stride_qkv, c->rope, c->hq, c->hkv, c->hd, l, c->n_blocks, c->btab, c->MAXB,
+                       c->PB, (T*)c->qbuf, (T*)c->kc, (T*)c->vc);
+    PROF_E(c, kPQkv, c->nqkv, 0);
+    PROF_B(c);
+    hipLaunchKernelGGL((k_attention<T, HD>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
+                       M_ptr, c->rows, (const T*)c->qbuf, (const T*)c->kc, (const T*)c->vc, c->btab,
+                       c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv, c->attn_splits_max,
+                       1.0f / sqrtf((float)HD), c->attn_part);
+    PROF_E(c, kPAttn, 0, 0);
+    PROF_B(c);
+    hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(M_cap, c->hq), dim3(HD), 0, st, M_ptr, c->rows,
+                       c->attn_part, c->hq, c->hkv, c->attn_splits_max, x);
+    PROF_E(c, kPCombine, 0, 0);
+    PROF_B(c);
+    gemm(c, x, c->w_o[l], M_ptr, M_cap, d, c->qdim, sp);
+    PROF_E(c, kPGemm, d, c->qdim);
+    PROF_B(c);
+    hipLaunchKernelGGL(k_residual_norm<T>, dim3(M_cap), dim3(256), 0, st, M_ptr, c->ws, sp,
+                       (int64_t)M_cap * d, d, c->h, c->norms + (size_t)(2 * l + 1) * d,
+                       c->md.rms_eps, x);
+    PROF_E(c, kPResNorm, d, 0);
+    PROF_B(c);
+    gemm(c, x, c->w_gu[l], M_ptr, M_cap, 2 * c->ffn, d, sp);
+    PROF_E(c, kPGemm, 2 * c->ffn, d);
+    PROF_B(c);
+    hipLaunchKernelGGL(k_swiglu<T>, dim3((c->ffn + 255) / 256, M_cap), dim3(256), 0, st, M_ptr, c->ws,
+                       sp, (int64_t)M_cap * 2 * c->ffn, c->ffn, x);
+    PROF_E(c, kPSwiglu, c->ffn, 0);
+    PROF_B(c);
+    gemm(c, x, c->w_d[l], M_ptr, M_cap, d, c->ffn, sp);
+    PROF_E(c, kPGemm, d, c->ffn);
+    const float* nw = (l + 1 < c->L) ? c->norms + (size_t)(2 * (l + 1)) * d
+                                     : c->norms + (size_t)(2 * c->L) * d;
+    // the last layer's norm output is only needed when logits follow
+    if (l + 1 < c->L || final_norm_out) {
+      PROF_B(c);
+      hipLaunchKernelGGL(k_residual_norm<T>, dim3(M_cap), dim3(256), 0, st, M_ptr, c->ws, sp,
+                         (int64_t)M_cap * d, d, c->h, nw, c->md.rms_eps, x);
+      PROF_E(c, kPResNorm, d, 0);
+    }
+  }
+}
+
+template <typename T>
+static void layers(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_norm_out) {
+  if (c->hd == 128) layers_T<T, 128>(c, M_ptr, M_cap, final_norm_out);
+  else layers_T<T, 64>(c, M_ptr, M_cap, final_norm_out);
+}
+
+int launch_prefill(sara_ctx* c) {
+  hipStream_t st = c->stream;
+  // prefix sums of (P - 1): prompt-token rows of the pool, chunked
+  std::vector<int64_t> pre(c->U + 1, 0);
+  for (int u = 0; u < c->U; ++u) pre[u + 1] = pre[u] + (c->h_off[u + 1] - c->h_off[u] - 1);
+  int64_t rows_total = pre[c->U];
+  for (int64_t r0 = 0; r0 < rows_total; r0 += c->prefill_rows) {
+    int n = (int)((rows_total - r0 < c->prefill_rows) ? rows_total - r0 : c->prefill_rows);
+    hipLaunchKernelGGL(k_prefill_rows, dim3((n + 255) / 256), dim3(256), 0, st, c->pre, c->U, (int)r0,
+                       n, c->tok, c->off, c->S, c->rows, c->rows_M);
+    if (c->md.dtype == SARA_BF16) {
+      hipLaunchKernelGGL(k_embed_norm<uint16_t>, dim3(n), dim3(256), 0, st, c->rows_M, c->rows,
+                         (const uint16_t*)c->embed, c->norms, c->d, c->md.rms_eps, c->h,
+                         (uint16_t*)c->x);
+      layers<uint16_t>(c, c->rows_M, n, false);
+    } else {
+      hipLaunchKernelGGL(k_embed_norm<float>, dim3(n), dim3(256), 0, st, c->rows_M, c->rows,
+                         (const float*)c->embed, c->norms, c->d, c->md.rms_eps, c->h, (float*)c->x);
+      layers<float>(c, c->rows_M, n, false);
+    }
+  }
+  return SARA_OK;
+}
+
+int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_free) {
+  hipStream_t st = c->stream;
+  const int S = c->S;
+  PROF_B(c);
+  hipLaunchKernelGGL(k_decode_M, dim3(1), dim3(1), 0, st, c->ctl, c->rows_M);
+  hipLaunchKernelGGL(k_decode_rows, dim3((S + 255) / 256), dim3(256), 0, st, c->ctl, c->active,
+                     c->slot_uid, c->slot_j, c->slot_gen, c->tok, c->off, c->out_tok, c->k,
+                     c->ad.max_new, c->rows);
+  PROF_E(c, kPRows, 0, 0);
+  if (!model_free) {
+    PROF_B(c);
+    if (c->md.dtype == SARA_BF16)
+      hipLaunchKernelGGL(k_embed_norm<uint16_t>, dim3(S), dim3(256), 0, st, c->rows_M, c->rows,
+                         (const uint16_t*)c->embed, c->norms, c->d, c->md.rms_eps, c->h,
+                         (uint16_t*)c->x);
+    else
+      hipLaunchKernelGGL(k_embed_norm<float>, dim3(S), dim3(256), 0, st, c->rows_M, c->rows,
+                         (const float*)c->embed, c->norms, c->d, c->md.rms_eps, c->h, (float*)c->x);
+    PROF_E(c, kPEmbed, c->d, 0);
+    if (c->md.dtype == SARA_BF16) layers<uint16_t>(c, c->rows_M, S, true);
+    else layers<float>(c, c->rows_M, S, true);
+    int sp;
+    // one K split: ws then holds the logits [M][V] directly
+    PROF_B(c);
+    gemm(c, c->x, c->lm_head, c->rows_M, S, c->V, c->d, sp, 1);
+    PROF_E(c, kPGemm, c->V, c->d);
+    PROF_B(c);
+    hipLaunchKernelGGL(k_sample_partial, dim3(S, kSampleChunks), dim3(256), 0, st, c->rows_M,
+                       (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, c->ws, c->V,
+                       (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, c->samp_best, c->samp_idx);
+    PROF_E(c, kPSampleP, c->V, 0);
+    if (logits) {
+      PROF_B(c);
+      hipLaunchKernelGGL(k_copy_logits, dim3(64, S), dim3(256), 0, st, c->ctl, c->rows, c->ws, c->V,
+                         logits);
+      PROF_E(c, kPCopy, c->V, 0);
+    }
+  }
+  PROF_B(c);
+  hipLaunchKernelGGL(k_sample_final, dim3((S + 255) / 256), dim3(256), 0, st, c->ctl, c->rows,
+                     c->samp_best, c->samp_idx, forced, c->flen, model_free,
+                     (const CtlParams*)c->cp_dev, c->p, c->out_tok, c->samp_tok, c->slot_gen, c->slot_hash, c->fin,
+                     c->r_len, c->r_reward);
+  PROF_E(c, kPSampleF, 0, 0);
+  return SARA_OK;
+}
+
+int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* rid,
+                       const int32_t* pos, uint64_t seed, int step, float temp, int eos,
+                       uint32_t feos, int32_t* tok, hipStream_t st) {
+  float* best = nullptr;
+  int32_t* bidx = nullptr;
+  int32_t* mdev = nullptr;
+  hipError_t e = hipMallocAsync((void**)&best, sizeof(float) * (size_t)n_rows * kSampleChunks, st);
+  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
+  e = hipMallocAsync((void**)&bidx, sizeof(int32_t) * (size_t)n_rows * kSampleChunks, st);
+  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
+  e = hipMallocAsync((void**)&mdev, sizeof(int32_t), st);
+  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
+  e = hipMemcpyAsync(mdev, &n_rows, sizeof(int32_t), hipMemcpyHostToDevice, st);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  hipLaunchKernelGGL(k_sample_partial, dim3(n_rows, kSampleChunks), dim3(256), 0, st, mdev, rid, pos,
+                     (const RowDesc*)nullptr, logits, V, (const CtlParams*)nullptr, seed, step, temp,
+                     best, bidx);
+  hipLaunchKernelGGL(k_sample_rows_final, dim3((n_rows + 255) / 256), dim3(256), 0, st, n_rows, rid,
+                     pos, best, bidx, seed, step, eos, feos, tok);
+  (void)hipFreeAsync(best, st);
+  (void)hipFreeAsync(bidx, st);
+  (void)hipFreeAsync(mdev, st);
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "sample_rows");
+  return SARA_OK;
+}
+
+// norm weights -> fp32 [2L+1][d]
+__global__ void k_norm_to_f32_bf16(const uint16_t* __restrict__ src, float* __restrict__ dst, int d) {
+  int c = blockIdx.x * 256 + threadIdx.x;
+  if (c < d) dst[c] = bf16_to_f32(src[c]);
+}
+
+int launch_convert_norms(sara_ctx* c, const void* const* w) {
+  const int d = c->d;
+  for (int l = 0; l <= 2 * c->L; ++l) {
+    const void* src;
+    if (l == 2 * c->L) src = w[1 + 9 * c->L];
+    else src = w[1 + 9 * (l / 2) + ((l & 1) ? 5 : 0)];
+    float* dst = c->norms + (size_t)l * d;
+    if (c->md.dtype == SARA_BF16)
+      hipLaunchKernelGGL(k_norm_to_f32_bf16, dim3((d + 255) / 256), dim3(256), 0, c->stream,
+                         (const uint16_t*)src, dst, d);
+    else {
+      hipError_t e = hipMemcpyAsync(dst, src, sizeof(float) * d, hipMemcpyDeviceToDevice, c->stream);
+      if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync norms");
+    }
+  }
+  return SARA_OK;
+}
+
+}  // namespace sara

@@ -1,0 +1,252 @@
+// Internal declarations of libsara (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/sara.h"
+
+namespace sara {
+
+// ---------------------------------------------------------------------------
+// constants
+// ---------------------------------------------------------------------------
+constexpr int kBlockTok = 16;        // KV page size in tokens
+constexpr int kAttnSplit = 512;      // tokens per attention context split
+constexpr int kAttnTile = 64;        // tokens per LDS tile inside a split
+constexpr int kSampleChunks = 16;    // vocabulary chunks per sampled row
+constexpr int kCtlThreads = 1024;    // threads of the single-workgroup controller
+constexpr int kMaxQueue = 4096;      // pending rollouts held in LDS by the refill
+constexpr int kMaxSlots = 4096;
+constexpr int kMaxGroup = 8;         // query heads per KV head
+constexpr uint64_t kSeedRXor = 0xD1B54A32D192ED03ull;
+
+// ---------------------------------------------------------------------------
+// device-side state
+// ---------------------------------------------------------------------------
+struct Ctl {
+  int64_t budget_left, rollouts, tokens;
+  int64_t n_dec, n_draw, n_asg, n_fin;
+  int32_t next_uid, nA, nC, nAb;
+  int32_t qlen, t, done, error;
+  int32_t M, dirty, running, pad_;
+};
+
+// One query row of a decode or prefill batch.
+struct RowDesc {
+  int32_t tok;      // input token id
+  int32_t pos;      // position of the token (KV append position)
+  int32_t plen;     // tokens of the sequence's shared prompt segment (P - 1)
+  int32_t tab;      // block-table row
+  int32_t slot;     // decode: slot index; prefill: -1
+  int32_t rid;      // decode: rollout id uid*k + j
+  int32_t gen;      // decode: generated index i
+  int32_t uid;
+};
+
+// Parameters every controller kernel reads.
+struct CtlParams {
+  int32_t B, k, n0, commit_min, U, S, mode, bits, max_new, PB, SB, MAXB, eos, Qcap;
+  double tau, a0, b0, prior;
+  uint64_t seed;
+  int32_t step;
+  uint32_t forced_eos;
+  float temperature;
+  int32_t has_flen;
+};
+
+}  // namespace sara
+
+// ---------------------------------------------------------------------------
+// host-side context
+// ---------------------------------------------------------------------------
+struct sara_ctx {
+  sara_model_desc md;
+  sara_alloc_desc ad;
+  hipStream_t stream = nullptr;
+  int device = 0;
+
+  // derived sizes
+  int L = 0, d = 0, hq = 0, hkv = 0, hd = 0, ffn = 0, V = 0, G = 0, nqkv = 0, qdim = 0;
+  int U = 0, k = 0, S = 0, PB = 0, SB = 0, MAXB = 0, max_pos = 0, Qcap = 0;
+  int64_t n_blocks = 0;
+  int elt = 2;                    // bytes per stored element (2 bf16, 4 fp32)
+  int prefill_rows = 0;           // rows per prefill chunk
+  int attn_splits_max = 0;
+  int64_t ws_floats = 0;
+
+  // weights (model dtype)
+  void* embed = nullptr;
+  void* lm_head = nullptr;
+  std::vector<void*> w_qkv, w_o, w_gu, w_d;
+  float* norms = nullptr;         // [2L+1][d]: attn l, ffn l, final
+
+  // KV cache [L][n_blocks][hkv][16][hd], block tables [(S+U)][MAXB]
+  void* kc = nullptr;
+  void* vc = nullptr;
+  int32_t* btab = nullptr;
+  float2* rope = nullptr;         // [max_pos][hd/2] (cos, sin)
+
+  // prompt pool (library copies)
+  int32_t* tok = nullptr;
+  int32_t* off = nullptr;         // [U+1]
+  int32_t* pre = nullptr;         // [U+1] prefix sums of (P - 1)
+  double* p = nullptr;
+  int32_t* flen = nullptr;        // [U*k]
+  int has_flen = 0;
+  int64_t tok_cap = 0;
+  std::vector<int32_t> h_off;
+
+  // controller state
+  sara::Ctl* ctl = nullptr;
+  int32_t *status = nullptr, *n_iss = nullptr, *n_done = nullptr, *succ = nullptr, *infl = nullptr;
+  double* peff = nullptr;
+  int32_t *slot_uid = nullptr, *slot_j = nullptr, *slot_gen = nullptr, *fin = nullptr;
+  uint64_t* slot_hash = nullptr;
+  int32_t* active = nullptr;
+  uint64_t* queue = nullptr;
+  int32_t *out_tok = nullptr, *samp_tok = nullptr, *r_len = nullptr, *r_reward = nullptr;
+  int64_t *log_dec = nullptr, *log_draw = nullptr, *log_asg = nullptr, *log_fin = nullptr;
+  int64_t cap_dec = 0, cap_draw = 0, cap_asg = 0, cap_fin = 0;
+
+  // activations and workspaces
+  sara::RowDesc* rows = nullptr;  // [row_cap]
+  int32_t* rows_M = nullptr;      // device row count of the prefill chunk
+  int row_cap = 0;
+  float* h = nullptr;             // [row_cap][d] residual stream
+  void* x = nullptr;              // [row_cap][max(d, ffn, qdim)] GEMM input (model dtype)
+  void* qbuf = nullptr;           // [row_cap][hq][hd]
+  float* ws = nullptr;            // GEMM partial outputs
+  float* attn_part = nullptr;
+  float* samp_best = nullptr;
+  int32_t* samp_idx = nullptr;
+
+  // GRPO of committed groups
+  int32_t* g_off = nullptr;
+  float* g_r = nullptr;
+  float* g_adv = nullptr;
+  int32_t* g_n = nullptr;         // committed count used for the CSR
+
+  // graph replay
+  hipGraphExec_t graph_exec = nullptr;
+  hipGraph_t graph = nullptr;
+  int graph_iters = 0;
+  const int32_t* graph_forced = nullptr;
+  int32_t* h_done = nullptr;      // pinned
+
+  std::vector<void*> owned;       // device allocations freed by sara_destroy
+  // per-launch profiling of eager decode steps
+  struct ProfRec { int cls, N, K, e0, e1; };
+  bool prof_enabled = false;
+  bool prof_active = false;
+  bool capturing = false;
+  std::vector<hipEvent_t> prof_events;
+  std::vector<ProfRec> prof_recs;
+  int prof_next_event = 0;
+  std::vector<sara_kernel_profile> prof_tot;
+  sara::CtlParams cp;              // host copy
+  sara::CtlParams* cp_dev = nullptr;
+  int step_index = 0;
+  bool in_step = false;
+};
+
+namespace sara {
+
+enum ProfClass { kPGemm, kPAttn, kPCombine, kPQkv, kPResNorm, kPSwiglu, kPEmbed, kPSampleP,
+                 kPSampleF, kPRows, kPCopy, kPNumClasses };
+extern const char* const kProfNames[kPNumClasses];
+void prof_begin(sara_ctx* c);
+void prof_end(sara_ctx* c, int cls, int N = 0, int K = 0);
+int prof_collect(sara_ctx* c);
+
+void set_error(const std::string& msg);
+int hip_fail(hipError_t e, const char* what);
+
+// launchers (model)
+int launch_prefill(sara_ctx* c);
+int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_free);
+// launchers (controller)
+int launch_reset(sara_ctx* c);
+int launch_decide(sara_ctx* c);
+int launch_refill(sara_ctx* c);
+int launch_finish(sara_ctx* c, float eps);
+int launch_peff(const int32_t* n, const int32_t* s, int k, double a0, double b0, int count,
+                double* out, hipStream_t st);
+int launch_grpo(const float* r, const int32_t* off, int n_groups, float eps, float* adv,
+                hipStream_t st);
+int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* rid,
+                       const int32_t* pos, uint64_t seed, int step, float temp, int eos,
+                       uint32_t feos, int32_t* tok, hipStream_t st);
+int launch_convert_norms(sara_ctx* c, const void* const* w);
+
+// ---------------------------------------------------------------------------
+// device helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(((uint32_t)b) << 16);
+}
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t b = __float_as_uint(f);
+  return (uint16_t)((b + 0x7FFFu + ((b >> 16) & 1u)) >> 16);
+}
+template <typename T> __device__ __forceinline__ float ld_f32(const T* p, size_t i);
+template <> __device__ __forceinline__ float ld_f32<float>(const float* p, size_t i) { return p[i]; }
+template <> __device__ __forceinline__ float ld_f32<uint16_t>(const uint16_t* p, size_t i) {
+  return bf16_to_f32(p[i]);
+}
+template <typename T> __device__ __forceinline__ void st_f32(T* p, size_t i, float v);
+template <> __device__ __forceinline__ void st_f32<float>(float* p, size_t i, float v) { p[i] = v; }
+template <> __device__ __forceinline__ void st_f32<uint16_t>(uint16_t* p, size_t i, float v) {
+  p[i] = f32_to_bf16(v);
+}
+
+// Philox4x32-10 (Salmon et al., SC'11): 10 rounds of two 32x32->64 products
+// and a Weyl-sequence key schedule.
+struct U32x4 { uint32_t x, y, z, w; };
+__device__ __forceinline__ U32x4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
+                                               uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
+    uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
+    uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+    uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
+  }
+  return U32x4{c0, c1, c2, c3};
+}
+__device__ __forceinline__ void sampler_key(uint64_t seed, int32_t step, uint32_t& k0, uint32_t& k1) {
+  k0 = (uint32_t)seed;
+  k1 = (uint32_t)(seed >> 32) ^ (uint32_t)step;
+}
+
+// SplitMix64 output finalizer (Steele, Lea, Flood, OOPSLA'14).
+__host__ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+__device__ __forceinline__ uint64_t reward_hash_init(uint64_t seed, int32_t step, int32_t uid) {
+  return mix64((seed ^ kSeedRXor) ^ mix64(((uint64_t)(uint32_t)step << 32) + (uint64_t)(uint32_t)uid));
+}
+
+// Proposition 1 (Eq. peff): posterior predictive probability that the
+// completed group of size k is mixed, given n observed rollouts with s
+// successes under the prior Beta(a0, b0).  Both saturation terms apply when
+// n = 0; a complete unmixed group has probability 0.
+__device__ __forceinline__ double peff_dev(int n, int s, int k, double a0, double b0) {
+  if (s >= 1 && n - s >= 1) return 1.0;
+  int r = k - n;
+  if (r <= 0) return 0.0;
+  double a = a0 + (double)s, b = b0 + (double)(n - s);
+  double lb = lgamma(a) + lgamma(b) - lgamma(a + b);
+  double psat = 0.0;
+  if (s == 0) psat += exp(lgamma(a) + lgamma(b + r) - lgamma(a + b + r) - lb);
+  if (s == n) psat += exp(lgamma(a + r) + lgamma(b) - lgamma(a + b + r) - lb);
+  return 1.0 - psat;
+}
+
+}  // namespace sara

@@ -1,0 +1,221 @@
+"""GPU-vs-oracle parity through the C ABI (needs an MI355X)."""
+import math
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import controller as OC
+from oracle import grpo as OG
+from oracle import predictor as OP
+from oracle import run as ORUN
+from oracle import sampler as OS
+from tests.gpu_harness import compare_logs, device_setup, forced_table, run_gpu_step, slot_rows
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+    import paper_2607_26253_amd  # noqa: F401  (fails loudly when libsara.so is missing)
+    return torch
+
+
+def test_peff_batch_matches_oracle(torch_cuda):
+    import paper_2607_26253_amd as sara
+    torch = torch_cuda
+    for (k, a0, b0) in [(8, 1.0, 1.0), (8, 0.3, 3.0), (16, 2.5, 0.7), (2, 1.0, 1.0), (31, 0.05, 7.5)]:
+        ns, ss = [], []
+        for n in range(0, k + 1):
+            for s in range(0, n + 1):
+                ns.append(n)
+                ss.append(s)
+        d_n = torch.tensor(ns, dtype=torch.int32, device="cuda")
+        d_s = torch.tensor(ss, dtype=torch.int32, device="cuda")
+        out = torch.empty(len(ns), dtype=torch.float64, device="cuda")
+        sara.sara_peff_batch(d_n, d_s, k, a0, b0, out)
+        got = out.cpu().numpy()
+        want = np.array([OP.p_eff(n, s, k, a0, b0) for n, s in zip(ns, ss)])
+        assert np.max(np.abs(got - want)) <= 1e-12
+
+
+def test_grpo_matches_oracle(torch_cuda):
+    import paper_2607_26253_amd as sara
+    torch = torch_cuda
+    g = np.random.default_rng(0)
+    sizes = [8, 8, 1, 0, 5, 64, 130, 2, 8]
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    r = np.where(g.random(off[-1]) < 0.4, 1.0, 0.0).astype(np.float32)
+    r[8:16] = 1.0   # saturated group
+    d_r, d_off = torch.from_numpy(r).cuda(), torch.from_numpy(off).cuda()
+    d_a = torch.full((len(r),), 7.0, dtype=torch.float32, device="cuda")
+    sara.grpo_group_advantages(d_r, d_off, 1e-6, d_a)
+    got = d_a.cpu().numpy()
+    want = OG.advantages(r, off, 1e-6)
+    assert np.allclose(got, want, rtol=1e-6, atol=1e-6)
+    assert np.all(got[8:16] == 0.0)
+
+
+@pytest.mark.parametrize("V", [512, 151936])
+def test_sampler_on_oracle_logits(torch_cuda, V):
+    import paper_2607_26253_amd as sara
+    torch = torch_cuda
+    g = np.random.default_rng(V)
+    n = 48
+    logits = (g.standard_normal((n, V)) * 0.8).astype(np.float32)
+    rid = np.arange(n, dtype=np.int32) * 3 + 1
+    pos = (np.arange(n, dtype=np.int32) * 7) % 1024
+    seed, step = W.sampling_seed(W.get_config("qwen1p5b_shape")), 5
+    for temp, eos, feos in [(1.0, -1, 0), (0.7, V - 1, (1 << 32) // 16)]:
+        d_tok = torch.empty(n, dtype=torch.int32, device="cuda")
+        sara.sara_sample_logits(torch.from_numpy(logits).cuda(), torch.from_numpy(rid).cuda(),
+                                torch.from_numpy(pos).cuda(), seed, step, temp, eos, feos, d_tok)
+        got = d_tok.cpu().numpy()
+        ties = 0
+        for i in range(n):
+            tok, sc = OS.sample(logits[i], temp, seed, step, int(rid[i]), int(pos[i]))
+            if eos >= 0 and OS.forced_eos(seed, step, int(rid[i]), int(pos[i]), feos):
+                tok = eos
+            if got[i] != tok:
+                assert OS.near_tie(sc), (i, got[i], tok)
+                ties += 1
+        assert ties <= 1
+
+
+def _tiny():
+    cfg = W.get_config("tiny_f32")
+    w = W.make_weights(cfg)
+    pool = W.make_pool(cfg, 0)
+    seed = W.sampling_seed(cfg)
+    return cfg, w, pool, seed
+
+
+@pytest.fixture(scope="module")
+def tiny_oracle():
+    cfg, w, pool, seed = _tiny()
+    res = ORUN.run_step(cfg, w, pool, seed, keep_logits=lambda u, j, i: True)
+    return cfg, w, pool, seed, res
+
+
+def test_tiny_teacher_forced_logits_tokens_and_decisions(torch_cuda, tiny_oracle):
+    cfg, w, pool, seed, ora = tiny_oracle
+    ctx, _ = device_setup(cfg, w)
+    forced = forced_table(cfg, ora["rollouts_detail"])
+    gpu = run_gpu_step(ctx, cfg, pool, forced=forced, capture_logits=True)
+    # decisions, draws, assignments, finishes: bit-exact
+    compare_logs(gpu["logs"], ora)
+    st = gpu["stats"]
+    assert (st["committed"], st["rollouts"], st["tokens"], st["decode_steps"]) == (
+        ora["n_committed"], ora["rollouts"], ora["tokens"], ora["decode_steps"])
+    # logits of every occupied slot at every step: max |d| <= 1e-3 (fp32 model)
+    rows = slot_rows(gpu)
+    worst = 0.0
+    for (t, s), (u, j, i) in rows.items():
+        gl = gpu["logits"][t][s]
+        ol = ora["logits"][(u, j, i)]
+        worst = max(worst, float(np.max(np.abs(gl - ol))))
+    assert worst <= 1e-3, worst
+    # the sampler's own choice equals the oracle token except at near ties
+    k = cfg["alloc"]["k"]
+    ties = 0
+    for (u, j), d in ora["rollouts_detail"].items():
+        got = gpu["roll"]["sampled"][u * k + j][:d["length"]]
+        diff = np.nonzero(got != d["tokens"])[0]
+        ties += len(diff)
+    assert ties <= 2
+    # rewards and GRPO advantages
+    for (u, j), d in ora["rollouts_detail"].items():
+        assert gpu["roll"]["reward"][u * k + j] == d["reward"]
+        assert gpu["roll"]["length"][u * k + j] == d["length"]
+    off, r, a = gpu["adv"]
+    assert np.array_equal(off, ora["grpo_offsets"])
+    assert np.array_equal(r, ora["grpo_rewards"])
+    assert np.allclose(a, ora["advantages"], rtol=1e-6, atol=1e-6)
+    ctx.close()
+
+
+def test_tiny_free_running_matches_oracle(torch_cuda, tiny_oracle):
+    cfg, w, pool, seed, ora = tiny_oracle
+    ctx, _ = device_setup(cfg, w)
+    gpu = run_gpu_step(ctx, cfg, pool, use_graph=True)
+    k = cfg["alloc"]["k"]
+    diverged = False
+    for (u, j), d in ora["rollouts_detail"].items():
+        got = gpu["roll"]["tokens"][u * k + j][:d["length"]]
+        if not np.array_equal(got, d["tokens"]):
+            diverged = True
+    if not diverged:
+        compare_logs(gpu["logs"], ora)
+    else:
+        pytest.fail("free-running GPU tokens diverged from the oracle")
+    ctx.close()
+
+
+def _model_free_case(cfg, U_tokens_seed=3):
+    a = cfg["alloc"]
+    U, k, mn = a["pool_U"], a["k"], a["max_new"]
+    g = np.random.default_rng(U_tokens_seed)
+    V = cfg["model"]["vocab"]
+    tab = g.integers(0, V, size=(U * k, mn)).astype(np.int32)
+    return tab
+
+
+@pytest.mark.parametrize("name,mode", [("qwen1p5b_shape", "sara"), ("long_ragged_1p5b", "sara"),
+                                       ("pool_3b", "sara"), ("pool_3b", "fixed_k"),
+                                       ("qwen3b_shape", "sara")])
+def test_controller_full_size_model_free(torch_cuda, name, mode):
+    """Full-size allocation parameters of each workload; tokens from a table
+    (decoder skipped), so the controller, hash reward and termination are
+    checked bit-exactly against the oracle's event simulation."""
+    full = W.get_config(name)
+    if mode == "fixed_k":
+        full = W.fixed_k_variant(full)
+    cfg = W.get_config("tiny_f32")
+    cfg["alloc"] = dict(full["alloc"])
+    cfg["alloc"]["max_prompt"] = 32
+    cfg["model"]["eos_id"] = 511
+    cfg["forced_len"] = full["forced_len"]
+    cfg["index"] = full["index"]
+    cfg["steps"] = full["steps"]
+    cfg["mixture"] = full["mixture"]
+    cfg["prompt_len"] = (8, 32)
+    a = cfg["alloc"]
+    a["max_new"] = min(a["max_new"], 96)
+    if cfg["forced_len"] is not None:
+        cfg["forced_len"] = dict(cfg["forced_len"], cap=a["max_new"], mu=math.log(40.0))
+    pool = W.make_pool(cfg, 0)
+    tab = _model_free_case(cfg)
+    # EOS in the table ends rollouts early: sprinkle it with probability 1/40
+    g = np.random.default_rng(9)
+    tab[g.random(tab.shape) < 1 / 40] = 511
+    w = W.make_weights(W.get_config("tiny_f32"))
+    ctx, _ = device_setup(cfg, w)
+    gpu = run_gpu_step(ctx, cfg, pool, forced=tab, model_free=True)
+    seed = W.sampling_seed(cfg)
+    ora = ORUN.run_step(cfg, None, pool, seed, forced_tokens=tab, model_free=True)
+    compare_logs(gpu["logs"], ora)
+    st = gpu["stats"]
+    assert (st["committed"], st["rollouts"], st["tokens"], st["decode_steps"], st["budget_left"]) == (
+        ora["n_committed"], ora["rollouts"], ora["tokens"], ora["decode_steps"], ora["budget_left"])
+    off, r, adv = gpu["adv"]
+    assert np.array_equal(off, ora["grpo_offsets"])
+    assert np.allclose(adv, ora["advantages"], rtol=1e-6, atol=1e-6)
+    ctx.close()
+
+
+def test_saturated_pool_abandoned_after_probe(torch_cuda):
+    cfg = W.get_config("tiny_f32")
+    cfg["alloc"].update(B=64, budget_N=512, n_slots=512, pool_U=256)
+    pool = W.saturated_pool(W.make_pool(cfg, 0))
+    tab = _model_free_case(cfg)
+    w = W.make_weights(W.get_config("tiny_f32"))
+    ctx, _ = device_setup(cfg, w)
+    gpu = run_gpu_step(ctx, cfg, pool, forced=tab, model_free=True)
+    ro = gpu["roll"]
+    drawn = gpu["stats"]["drawn"]
+    assert gpu["stats"]["committed"] == 0
+    assert np.all(ro["status"][:drawn] == 3) and np.all(ro["n"][:drawn] == 4)
+    assert gpu["stats"]["rollouts"] == 4 * drawn
+    ctx.close()
