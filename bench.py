@@ -75,10 +75,11 @@ def cpu_baseline(cfg, weights, seconds_target=15.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2)
+    ap.add_argument("--steps", type=int, default=1)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="qwen1p5b_shape")
     ap.add_argument("--graph-iters", type=int, default=16)
+    ap.add_argument("--chunk-iters", type=int, default=2048)
     ap.add_argument("--profile-every", type=int, default=16)
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -115,15 +116,23 @@ def main():
         pools.append((p, d_tok, d_p, d_fl))
     torch.cuda.synchronize()
 
-    def one_step(i):
+    def one_step(i, tag):
         p, d_tok, d_p, d_fl = pools[i]
         ctx.sara_begin_step(d_tok, p["offsets"], d_p, d_fl, p["step"])
-        ctx.sara_run(None, graph_iters=args.graph_iters)
+        iters = 0
+        while True:
+            # replay the decode/decide/refill graph in chunks; each chunk reports progress
+            iters += ctx.sara_run(None, graph_iters=args.graph_iters, max_iters=args.chunk_iters)
+            q = ctx.sara_query()
+            print(f"[bench] {tag}: {iters} loop iterations, {q['tokens']} tokens, {q['committed']} committed",
+                  file=sys.stderr, flush=True)
+            if q["done"]:
+                break
         ctx.sara_finish_step(1e-6)
         return ctx.sara_query()
 
     for i in range(args.warmup):
-        st = one_step(i)
+        st = one_step(i, f"warmup {i}")
         print(f"[bench] warmup step {i}: {st['tokens']} tokens, {st['decode_steps']} decode steps",
               file=sys.stderr, flush=True)
 
@@ -131,7 +140,7 @@ def main():
     stats = []
     t0 = time.perf_counter()
     for i in range(args.steps):
-        stats.append(one_step(args.warmup + i))
+        stats.append(one_step(args.warmup + i, f"step {i}"))
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     for i, st in enumerate(stats):
@@ -165,6 +174,8 @@ def main():
         while True:
             if it % 16 == 0 and ctx.sara_query()["done"]:
                 break
+            if it % 2048 == 0:
+                print(f"[bench] profiled pass: {it} decode steps", file=sys.stderr, flush=True)
             on = (it % args.profile_every) == 0
             ctx.sara_set_profiling(on)
             ctx.sara_decode_step(None, None, False)
@@ -175,7 +186,8 @@ def main():
         ctx.sara_set_profiling(False)
         prof = ctx.sara_read_profile()
         tprof = time.perf_counter() - tprof
-        dec = [k for k in prof if k["launches"] > 0]
+        allc = [k for k in prof if k["launches"] > 0]
+        dec = [k for k in allc if not k["name"].startswith(".")]      # kernels (no sub-classes)
         tot_ms = sum(k["ms"] for k in dec)
         tot_by = sum(k["bytes"] for k in dec)
         dom = max(dec, key=lambda k: k["ms"])
@@ -195,8 +207,9 @@ def main():
             "decode_hbm_gbs": tot_by / (tot_ms * 1e-3) / 1e9,
             "decode_hbm_frac": tot_by / (tot_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "classes": {k["name"]: {"launches": k["launches"], "ms": round(k["ms"], 3),
+                                    "avg_us": round(1e3 * k["ms"] / k["launches"], 2),
                                     "GBps": round(k["bytes"] / (k["ms"] * 1e-3) / 1e9, 1) if k["ms"] else None}
-                        for k in dec},
+                        for k in allc},
             "wall_s": tprof,
         }
         print(f"[bench] profiled {n_prof} of {it} decode steps; dominant {dom['name']}: {ach:.0f} GB/s; "

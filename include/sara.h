@@ -50,7 +50,7 @@ enum { SARA_UNDRAWN = 0, SARA_ACTIVE = 1, SARA_COMMITTED = 2, SARA_ABANDONED = 3
 /* Decoder shape.  Pre-norm GQA decoder: RMSNorm, rotate-half RoPE, SwiGLU,
  * untied LM head, no biases.  head_dim in {64, 128}; n_heads a multiple of
  * n_kv_heads with at most 8 query heads per KV head; d_model, d_ffn and
- * n_heads*head_dim multiples of 32.  dtype SARA_BF16 stores weights, KV cache
+ * n_heads*head_dim multiples of 64; vocab a multiple of 16.  dtype SARA_BF16 stores weights, KV cache
  * and GEMM inputs in bf16 (fp32 accumulation); SARA_F32 computes in fp32.
  * eos_id = -1 disables the EOS token. */
 typedef struct {

@@ -17,10 +17,13 @@
 
 #include <math.h>
 
+#include <algorithm>
+
 namespace sara {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------------------
 // block reductions (fixed tree order -> deterministic)
@@ -124,66 +127,138 @@ __global__ __launch_bounds__(256) void k_embed_norm(const int32_t* __restrict__ 
 // ---------------------------------------------------------------------------
 // GEMM: out[s][m][n] = sum_{k in split s} X[m][k] * W[n][k]
 // ---------------------------------------------------------------------------
-// bf16 MFMA.  A wave owns 16 weight rows (n) and MT tiles of 16 activation
-// rows (m).  Both operands are read straight from global memory in the MFMA
-// operand layout: lane l supplies row (l % 16) and the 8 consecutive k of
-// k-group (l / 16); the k-groups of the two operands coincide, so the
-// product is exact for any assignment of k to groups.  A 128-wide k step
-// loads 64 B per lane per row (256 B contiguous per row per wave).
-template <int MT>
-__global__ __launch_bounds__(256) void k_gemm_bf16(const uint16_t* __restrict__ X,
-    const uint16_t* __restrict__ W, float* __restrict__ out, const int32_t* __restrict__ M_ptr,
+// bf16 MFMA GEMM with the activation tile in LDS.  Block = 4 waves; wave w
+// owns weight rows [n0, n0 + 16*NT) and all 16*MT activation rows of the
+// block's m-range.  The k loop is a 4-slot software pipeline: stage s loads
+// the X chunk (block-cooperative) and the wave's W chunk for k chunk s into
+// register slot s % 4, three stages ahead of its use; at its turn the X
+// chunk is written to one of two LDS buffers, and the MFMAs read X from LDS
+// and W from registers.  Loads of one stage are issued together, so waiting
+// for the oldest stage leaves the three younger ones in flight.
+//
+// EPI = 0: fp32 partial sums to out[split][m][n].
+// EPI = 1: SwiGLU epilogue (one split only): the weight rows are interleaved
+//          per 16-row tile as gate (even tiles) and up (odd tiles) of the same
+//          16 features; out receives bf16 silu(g) * u as [m][N/2].
+template <int NT, int MT, int KC, int EPI>
+__global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __restrict__ X,
+    const uint16_t* __restrict__ W, void* __restrict__ out, const int32_t* __restrict__ M_ptr,
     int N, int K, int kps, int64_t split_stride) {
+  constexpr int MR = 16 * MT;
+  constexpr int PITCH = KC + 8;                 // halves: rows shift by 4 banks, conflict-free b128 reads
+  constexpr int XU = MR * (KC / 8) / 256;       // uint4 per thread per X chunk
+  constexpr int CPK = KC / 32;                  // 16x16x32 MFMA k steps per chunk
+  constexpr int C8 = KC / 8;                    // uint4 per X row per chunk
+  constexpr int RING = 4;
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2][MR * PITCH];
   const int M = *M_ptr;
-  const int m_base = blockIdx.z * 16 * MT;
+  const int m_base = blockIdx.z * MR;
   if (m_base >= M) return;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int n0 = (blockIdx.x * 4 + wave) * 16;
-  if (n0 >= N) return;
   const int row = lane & 15, grp = lane >> 4;
+  const int n0 = (blockIdx.x * 4 + wave) * 16 * NT;
   const int k_begin = blockIdx.y * kps;
   const int k_end = min(K, k_begin + kps);
-  const uint16_t* wrow = W + (size_t)(n0 + row) * K + 8 * grp;
-  const uint16_t* xrow[MT];
+  const int nchunks = (k_end - k_begin) / KC;
+  // element offsets (32-bit: rows * K < 2^31 for every supported shape)
+  int woff[NT];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    int m = min(m_base + 16 * t + row, M - 1);
-    xrow[t] = X + (size_t)m * K + 8 * grp;
+  for (int nt = 0; nt < NT; ++nt) woff[nt] = min(n0 + 16 * nt + row, N - 1) * K + 8 * grp + k_begin;
+  int xoff[XU], xdst[XU];
+#pragma unroll
+  for (int q = 0; q < XU; ++q) {
+    int u = threadIdx.x + 256 * q;
+    int rr = u / C8, c8 = u % C8;
+    xoff[q] = min(m_base + rr, M - 1) * K + 8 * c8 + k_begin;
+    xdst[q] = rr * PITCH + 8 * c8;
   }
-  f32x4 acc[MT];
+  // the four pipeline slots are distinct variables (not an indexed array),
+  // so that they live in registers
+  struct Stage { u32x4 x[XU]; u32x4 w[NT][CPK]; };
+  Stage s0, s1, s2, s3;
+  f32x4 acc[NT][MT];
 #pragma unroll
-  for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  int kk = k_begin;
-  for (; kk + 128 <= k_end; kk += 128) {
-    uint4 wv[4];
+  for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) wv[c] = *(const uint4*)(wrow + kk + 32 * c);
+    for (int t = 0; t < MT; ++t) acc[nt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int last = max(nchunks - 1, 0);
+  // loads are unconditional (clamped to the last chunk); surplus loads are unused
+  auto load = [&](Stage& st, int chunk) {
+    const int kk = min(chunk, last) * KC;
 #pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      uint4 xv[4];
+    for (int q = 0; q < XU; ++q) st.x[q] = *(const u32x4*)(X + xoff[q] + kk);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) xv[c] = *(const uint4*)(xrow[t] + kk + 32 * c);
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
-        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wv[c]),
-                                                         __builtin_bit_cast(bf16x8, xv[c]), acc[t], 0, 0, 0);
+      for (int cc = 0; cc < CPK; ++cc) st.w[nt][cc] = *(const u32x4*)(W + woff[nt] + kk + 32 * cc);
+  };
+  auto consume = [&](Stage& st, int buf, int ch) {
+    // buffer `buf` was last read two chunks ago, before the previous barrier
+#pragma unroll
+    for (int q = 0; q < XU; ++q) *(u32x4*)&xs[buf][xdst[q]] = st.x[q];
+    __syncthreads();
+    if (ch < nchunks) {
+      // rows past M read a clamped (valid) X row; their results are never stored
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+#pragma unroll
+        for (int cc = 0; cc < CPK; ++cc) {
+          u32x4 xv = *(const u32x4*)&xs[buf][(16 * t + row) * PITCH + 8 * grp + 32 * cc];
+#pragma unroll
+          for (int nt = 0; nt < NT; ++nt)
+            acc[nt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, st.w[nt][cc]), __builtin_bit_cast(bf16x8, xv), acc[nt][t], 0, 0, 0);
+        }
+      }
     }
+  };
+  load(s0, 0);
+  load(s1, 1);
+  load(s2, 2);
+  for (int base = 0; base < nchunks; base += RING) {
+    load(s3, base + 3);
+    consume(s0, 0, base);
+    load(s0, base + 4);
+    consume(s1, 1, base + 1);
+    load(s1, base + 5);
+    consume(s2, 0, base + 2);
+    load(s2, base + 6);
+    consume(s3, 1, base + 3);
   }
-  for (; kk < k_end; kk += 32) {
-    uint4 wv = *(const uint4*)(wrow + kk);
+  if (EPI == 0) {
+    float* o = (float*)out + (size_t)blockIdx.y * split_stride;
 #pragma unroll
-    for (int t = 0; t < MT; ++t) {
-      uint4 xv = *(const uint4*)(xrow[t] + kk);
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, wv),
-                                                       __builtin_bit_cast(bf16x8, xv), acc[t], 0, 0, 0);
+    for (int nt = 0; nt < NT; ++nt) {
+      if (n0 + 16 * nt >= N) continue;
+#pragma unroll
+      for (int t = 0; t < MT; ++t) {
+        int m = m_base + 16 * t + row;
+        if (m < M) *(f32x4*)(o + (size_t)m * N + n0 + 16 * nt + 4 * grp) = acc[nt][t];
+      }
     }
-  }
-  // D[i][j]: i = weight row 4*grp + r, j = activation row (lane % 16)
-  float* o = out + (size_t)blockIdx.y * split_stride;
+  } else {
+    // tile pair (gate, up) = (nt 0, nt 1) of this wave: features (n0/32)*16 + 4*grp + q
+    uint16_t* o = (uint16_t*)out;
+    const int F = N / 2;
+    const int f0 = (n0 / 32) * 16 + 4 * grp;
+    if (n0 < N) {
 #pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    int m = m_base + 16 * t + row;
-    if (m < M) *(f32x4*)(o + (size_t)m * N + n0 + 4 * grp) = acc[t];
+      for (int t = 0; t < MT; ++t) {
+        int m = m_base + 16 * t + row;
+        if (m < M) {
+          uint32_t pk[2];
+#pragma unroll
+          for (int q = 0; q < 4; q += 2) {
+            float g0 = acc[0][t][q], u0 = acc[NT - 1][t][q];
+            float g1 = acc[0][t][q + 1], u1 = acc[NT - 1][t][q + 1];
+            float a0 = g0 / (1.0f + expf(-g0)) * u0;
+            float a1 = g1 / (1.0f + expf(-g1)) * u1;
+            pk[q / 2] = (uint32_t)f32_to_bf16(a0) | ((uint32_t)f32_to_bf16(a1) << 16);
+          }
+          *(uint2*)(o + (size_t)m * F + f0) = make_uint2(pk[0], pk[1]);
+        }
+      }
+    }
   }
 }
 
@@ -219,10 +294,22 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X,
 // ---------------------------------------------------------------------------
 // epilogues
 // ---------------------------------------------------------------------------
+// Sum of the split-K partials of one element in a fixed order (four running
+// sums over splits s = 0,4,8.. / 1,5,.. / 2,6,.. / 3,7,.. combined as
+// (a0 + a1) + (a2 + a3)): deterministic, with the loads issued together.
 __device__ __forceinline__ float split_sum(const float* ws, int splits, int64_t stride, size_t idx) {
-  float v = 0.f;
-  for (int s = 0; s < splits; ++s) v += ws[(size_t)s * stride + idx];
-  return v;
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+  int s = 0;
+  for (; s + 4 <= splits; s += 4) {
+    a0 += ws[(size_t)s * stride + idx];
+    a1 += ws[(size_t)(s + 1) * stride + idx];
+    a2 += ws[(size_t)(s + 2) * stride + idx];
+    a3 += ws[(size_t)(s + 3) * stride + idx];
+  }
+  if (s < splits) a0 += ws[(size_t)s * stride + idx];
+  if (s + 1 < splits) a1 += ws[(size_t)(s + 1) * stride + idx];
+  if (s + 2 < splits) a2 += ws[(size_t)(s + 2) * stride + idx];
+  return (a0 + a1) + (a2 + a3);
 }
 
 // Page of position pos: block-table entries [0, PB) map the shared prompt
@@ -238,6 +325,18 @@ __device__ __forceinline__ size_t kv_index(const RowDesc& r, const int32_t* btab
   return ((((size_t)layer * n_blocks + b) * hkv + g) * kBlockTok + o) * hd + dim;
 }
 
+// V pages are stored transposed, [hd][16 tokens] per (page, KV head), so that
+// the PV product reads 4 consecutive tokens of one dimension per lane.
+__device__ __forceinline__ size_t vt_index(const RowDesc& r, const int32_t* btab, int MAXB, int PB,
+                                           int layer, int64_t n_blocks, int hkv, int g, int hd,
+                                           int dim, int pos) {
+  int e, o;
+  if (pos < r.plen) { e = pos >> 4; o = pos & 15; }
+  else { int q = pos - r.plen; e = PB + (q >> 4); o = q & 15; }
+  int64_t b = btab[(size_t)r.tab * MAXB + e];
+  return ((((size_t)layer * n_blocks + b) * hkv + g) * hd + dim) * kBlockTok + o;
+}
+
 // Split-K sum of the fused q|k|v output, rotate-half RoPE on q and k,
 // q -> bf16 buffer, k and v -> the row's KV page.
 template <typename T>
@@ -246,12 +345,11 @@ __global__ __launch_bounds__(256) void k_qkv_epilogue(const int32_t* __restrict_
     const float2* __restrict__ rope, int hq, int hkv, int hd, int layer, int64_t n_blocks,
     const int32_t* __restrict__ btab, int MAXB, int PB, T* __restrict__ qbuf, T* __restrict__ kc,
     T* __restrict__ vc) {
-  int i = blockIdx.x;
-  if (i >= *M_ptr) return;
-  const RowDesc r = rows[i];
   const int half = hd >> 1, nh = hq + 2 * hkv, N = nh * hd;
-  for (int e = threadIdx.x; e < nh * half; e += 256) {
-    int h = e / half, c = e - h * half;
+  const int M = *M_ptr;
+  for (int item = blockIdx.x; item < M * nh; item += gridDim.x) {
+    const int i = item / nh, h = item - i * nh, c = threadIdx.x;
+    const RowDesc r = rows[i];
     size_t base = (size_t)i * N + (size_t)h * hd;
     float a = split_sum(ws, splits, stride, base + c);
     float b = split_sum(ws, splits, stride, base + c + half);
@@ -270,48 +368,57 @@ __global__ __launch_bounds__(256) void k_qkv_epilogue(const int32_t* __restrict_
       }
     } else {
       int g = h - hq - hkv;
-      st_f32(vc, kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, hd, c, r.pos), a);
-      st_f32(vc, kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, hd, c + half, r.pos), b);
+      st_f32(vc, vt_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, hd, c, r.pos), a);
+      st_f32(vc, vt_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, hd, c + half, r.pos), b);
     }
   }
 }
 
-// h += split-K sum; x = RMSNorm(h) * w  (stored in the model dtype)
+// h += split-K sum; x = RMSNorm(h) * w  (stored in the model dtype).
+// One 1024-thread block per row.
 template <typename T>
-__global__ __launch_bounds__(256) void k_residual_norm(const int32_t* __restrict__ M_ptr,
+__global__ __launch_bounds__(1024) void k_residual_norm(const int32_t* __restrict__ M_ptr,
     const float* __restrict__ ws, int splits, int64_t stride, int d, float* __restrict__ h,
     const float* __restrict__ w, float eps, T* __restrict__ x) {
-  __shared__ float red[4];
-  int i = blockIdx.x;
-  if (i >= *M_ptr) return;
+  __shared__ float red[16];
+  const int M = *M_ptr;
+  for (int i = blockIdx.x; i < M; i += gridDim.x) {
   float ss = 0.f;
-  for (int c = threadIdx.x; c < d; c += 256) {
+  for (int c = threadIdx.x; c < d; c += 1024) {
     size_t idx = (size_t)i * d + c;
     float v = h[idx] + split_sum(ws, splits, stride, idx);
     h[idx] = v;
     ss += v * v;
   }
-  float tot = block_sum256(ss, red);
+  ss = wave_sum(ss);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = ss;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int q = 0; q < 16; q += 4) tot += (red[q] + red[q + 1]) + (red[q + 2] + red[q + 3]);
   float inv = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int c = threadIdx.x; c < d; c += 256) {
+  for (int c = threadIdx.x; c < d; c += 1024) {
     size_t idx = (size_t)i * d + c;
     st_f32(x, idx, h[idx] * inv * w[c]);
   }
+  __syncthreads();   // red[] is reused by the next row
+  }
 }
 
-// a = silu(g) * u from the fused gate|up output ([m][2*ffn])
+// a = silu(g) * u from the fused gate|up output ([m][2*ffn]); grid-stride
+// over the M * ffn outputs of the live rows
 template <typename T>
 __global__ __launch_bounds__(256) void k_swiglu(const int32_t* __restrict__ M_ptr,
     const float* __restrict__ ws, int splits, int64_t stride, int ffn, T* __restrict__ a) {
-  int i = blockIdx.y;
-  if (i >= *M_ptr) return;
-  int f = blockIdx.x * 256 + threadIdx.x;
-  if (f >= ffn) return;
-  size_t base = (size_t)i * 2 * ffn;
-  float g = split_sum(ws, splits, stride, base + f);
-  float u = split_sum(ws, splits, stride, base + ffn + f);
-  float sg = g / (1.0f + expf(-g));
-  st_f32(a, (size_t)i * ffn + f, sg * u);
+  const size_t total = (size_t)(*M_ptr) * ffn;
+  for (size_t e = (size_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (size_t)gridDim.x * 256) {
+    size_t i = e / ffn, f = e - i * ffn;
+    size_t base = i * 2 * ffn;
+    float g = split_sum(ws, splits, stride, base + f);
+    float u = split_sum(ws, splits, stride, base + ffn + f);
+    float sg = g / (1.0f + expf(-g));
+    st_f32(a, e, sg * u);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -359,9 +466,8 @@ __global__ __launch_bounds__(256) void k_attention(const int32_t* __restrict__ M
     const int n = min(kAttnTile, t1 - ts);
     for (int e = tid; e < n * HD; e += 256) {
       int tk = e / HD, dd = e - tk * HD;
-      size_t idx = kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, dd, ts + tk);
-      k_s[tk][dd] = ld_f32(kc, idx);
-      v_s[tk][dd] = ld_f32(vc, idx);
+      k_s[tk][dd] = ld_f32(kc, kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, dd, ts + tk));
+      v_s[tk][dd] = ld_f32(vc, vt_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, dd, ts + tk));
     }
     __syncthreads();
     // scores: thread (token lane, head wave / wave + 4)
@@ -431,16 +537,166 @@ __global__ __launch_bounds__(256) void k_attention(const int32_t* __restrict__ M
   }
 }
 
+// bf16 paged GQA attention on the MFMA.  Block (row i, KV head g, split c)
+// covers KV pages [c*kAttnChunks, (c+1)*kAttnChunks) of the row's sequence
+// (prompt pages, then private pages; each page holds up to 16 positions);
+// its 4 waves take every 4th page.  Per page and wave:
+//   S^T = K q^T  (16 tokens x 16 padded heads, v_mfma_f32_16x16x32_bf16; the
+//                 lane supplying token l%16 of K and head l%16 of q reads the
+//                 same HD/4 dimensions, so the k order inside the MFMA is moot)
+//   online softmax per head (the 4 lanes holding one head's 16 scores)
+//   O += P V     (v_mfma_f32_16x16x16bf16_1k; the score registers are already
+//                 the A operand's layout, V^T pages give the B operand; P is
+//                 split into bf16 hi + lo parts, two MFMAs)
+// The 4 waves' (max, sum, O) are merged in LDS into one partial per split.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M_ptr,
+    const RowDesc* __restrict__ rows, const uint16_t* __restrict__ qbuf,
+    const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+    const int32_t* __restrict__ btab, int MAXB, int PB, int layer, int64_t n_blocks, int hq,
+    int hkv, int n_splits, float scale, float* __restrict__ part) {
+  typedef short short4_ __attribute__((ext_vector_type(4)));
+  constexpr int DPL = HD / 4;     // dims per lane in the QK^T operands
+  constexpr int NCC = HD / 32;    // 16x16x32 MFMAs per page for QK^T
+  constexpr int NT = HD / 16;     // output tiles of 16 dims
+  __shared__ float m_w[4][16], l_w[4][16];
+  __shared__ float o_w[4][16][HD + 1];
+  const int i = blockIdx.x, g = blockIdx.y, c = blockIdx.z;
+  if (i >= *M_ptr) return;
+  const RowDesc r = rows[i];
+  const int ctx = r.pos + 1;
+  const int pl = min(ctx, r.plen);                      // prompt positions attended
+  const int pc = (pl + 15) >> 4;                         // prompt pages
+  const int vcnt = ctx - pl;                             // private positions
+  const int nch = pc + ((vcnt + 15) >> 4);
+  const int ch0 = c * kAttnChunks;
+  if (ch0 >= nch) return;
+  const int ch1 = min(nch, ch0 + kAttnChunks);
+  const int G = hq / hkv;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = lane & 15, grp = lane >> 4;
+  // q operand: head `row` of this KV group (zero beyond G), dims [DPL*grp, DPL*grp + DPL)
+  uint4 qv[NCC];
+  if (row < G) {
+    const uint4* qp = (const uint4*)(qbuf + ((size_t)i * hq + g * G + row) * HD + DPL * grp);
+#pragma unroll
+    for (int cc = 0; cc < NCC; ++cc) qv[cc] = qp[cc];
+  } else {
+#pragma unroll
+    for (int cc = 0; cc < NCC; ++cc) qv[cc] = make_uint4(0, 0, 0, 0);
+  }
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 o[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int32_t* bt = btab + (size_t)r.tab * MAXB;
+  for (int ch = ch0 + wave; ch < ch1; ch += 4) {
+    int e, n;
+    if (ch < pc) { e = ch; n = min(16, pl - 16 * ch); }
+    else { int j = ch - pc; e = PB + j; n = min(16, vcnt - 16 * j); }
+    const size_t pg = ((size_t)layer * n_blocks + bt[e]) * hkv + g;
+    // S^T[token][head]
+    const uint4* kp = (const uint4*)(kc + (pg * kBlockTok + row) * HD + DPL * grp);
+    f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int cc = 0; cc < NCC; ++cc)
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kp[cc]),
+                                                   __builtin_bit_cast(bf16x8, qv[cc]), sc, 0, 0, 0);
+    // lane holds tokens 4*grp + q (q < 4) of head `row`
+    float sv[4];
+    float mt = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      sv[q] = (4 * grp + q < n) ? sc[q] * scale : -INFINITY;
+      mt = fmaxf(mt, sv[q]);
+    }
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float mn = fmaxf(m_run, mt);
+    const float alpha = expf(m_run - mn);
+    // P enters the MFMA as a bf16 pair hi + lo (|p - hi - lo| <= 2^-16 p), so
+    // the PV product keeps fp32 accuracy without a bf16 rounding point
+    float ps = 0.f;
+    uint16_t pb[4], pl[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float pv = expf(sv[q] - mn);
+      uint16_t b = f32_to_bf16(pv);
+      pb[q] = b;
+      pl[q] = f32_to_bf16(pv - bf16_to_f32(b));
+      ps += pv;
+    }
+    ps += __shfl_xor(ps, 16, 64);
+    ps += __shfl_xor(ps, 32, 64);
+    l_run = l_run * alpha + ps;
+    m_run = mn;
+    // rows of O are heads 4*grp + q: fetch their rescale factors
+    float al[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) al[q] = __shfl(alpha, 4 * grp + q, 64);
+    short4_ pa, pa_lo;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) { pa[q] = (short)pb[q]; pa_lo[q] = (short)pl[q]; }
+    const uint16_t* vp = vc + pg * (size_t)HD * kBlockTok + 4 * grp;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      uint2 vv = *(const uint2*)(vp + (size_t)(16 * t + row) * kBlockTok);
+      // positions beyond the page's n valid tokens may hold stale bits: zero them
+      short4_ vb;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t w = (q < 2) ? vv.x : vv.y;
+        uint16_t h = (uint16_t)((q & 1) ? (w >> 16) : (w & 0xFFFF));
+        vb[q] = (short)((4 * grp + q < n) ? h : (uint16_t)0);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[t][q] *= al[q];
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, vb, o[t], 0, 0, 0);
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa_lo, vb, o[t], 0, 0, 0);
+    }
+  }
+  // merge the 4 waves: lane `row` (grp 0) holds head row's (m, l); O rows are heads 4*grp + q
+  if (grp == 0) { m_w[wave][row] = m_run; l_w[wave][row] = l_run; }
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o_w[wave][4 * grp + q][16 * t + row] = o[t][q];
+  __syncthreads();
+  for (int e = threadIdx.x; e < G * HD; e += 256) {
+    int h = e / HD, dd = e - h * HD;
+    float mx = fmaxf(fmaxf(m_w[0][h], m_w[1][h]), fmaxf(m_w[2][h], m_w[3][h]));
+    float num = 0.f, den = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      float wt = (m_w[w][h] == -INFINITY) ? 0.f : expf(m_w[w][h] - mx);
+      num += wt * o_w[w][h][dd];
+      den += wt * l_w[w][h];
+    }
+    float* dst = part + ((((size_t)i * hkv + g) * n_splits + c) * kMaxGroup + h) * (HD + 2);
+    dst[dd] = num;
+    if (dd == 0) { dst[HD] = mx; dst[HD + 1] = den; }
+  }
+}
+
 // merge the context splits of every (row, query head) into o (model dtype)
 template <typename T, int HD>
 __global__ __launch_bounds__(HD) void k_attn_combine(const int32_t* __restrict__ M_ptr,
     const RowDesc* __restrict__ rows, const float* __restrict__ part, int hq, int hkv,
-    int n_splits, T* __restrict__ out) {
-  int i = blockIdx.x, h = blockIdx.y;
-  if (i >= *M_ptr) return;
+    int n_splits, int paged_splits, T* __restrict__ out) {
+  const int M = *M_ptr;
+  for (int item = blockIdx.x; item < M * hq; item += gridDim.x) {
+  const int i = item / hq, h = item - i * hq;
   int G = hq / hkv, g = h / G, gh = h - g * G;
-  int ctx = rows[i].pos + 1;
-  int ns = (ctx + kAttnSplit - 1) / kAttnSplit;
+  const RowDesc r = rows[i];
+  int ctx = r.pos + 1;
+  int ns;
+  if (paged_splits) {
+    int pl = min(ctx, r.plen);
+    int nch = ((pl + 15) >> 4) + ((ctx - pl + 15) >> 4);
+    ns = (nch + kAttnChunks - 1) / kAttnChunks;
+  } else {
+    ns = (ctx + kAttnSplit - 1) / kAttnSplit;
+  }
   const float* base = part + (((size_t)i * hkv + g) * n_splits * kMaxGroup + gh) * (HD + 2);
   const size_t sstride = (size_t)kMaxGroup * (HD + 2);
   float mx = -INFINITY;
@@ -453,6 +709,7 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const int32_t* __restrict__
     den += wgt * p[HD + 1];
   }
   st_f32(out, ((size_t)i * hq + h) * HD + threadIdx.x, num / den);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -613,20 +870,34 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
                 int N, int K, int& splits_out, int max_splits = 1 << 30) {
   int64_t stride = (int64_t)M_cap * N;
   if (c->md.dtype == SARA_BF16) {
+    // weight rows per block: 128 for very wide outputs (LM head), else 64;
+    // split K until the grid has about one block per CU (each split keeps
+    // >= 4 k chunks): wide GEMMs need no split, narrow ones trade fp32
+    // partial traffic for occupancy
     constexpr int MT = 8;
-    int tiles_n = (N + 63) / 64;
+    const bool wide = N >= 65536;
+    const int rows_per_block = wide ? 128 : 64;
+    int tiles_n = (N + rows_per_block - 1) / rows_per_block;
     int zb = (M_cap + 16 * MT - 1) / (16 * MT);
-    int want = (tiles_n * zb >= 512) ? 1 : (512 + tiles_n * zb - 1) / (tiles_n * zb);
-    int chunks = K / 32;
-    int splits = want < chunks ? want : chunks;
+    int want = (tiles_n >= 256) ? 1 : (256 + tiles_n - 1) / tiles_n;
+    // 64-wide k chunks: four pipeline slots of X + W fit in registers for NT <= 2
+    const int KC = 64;
+    int chunks = K / KC;
+    int splits = std::min(want, std::max(1, chunks / 4));
     if (splits > max_splits) splits = max_splits;
     if (splits < 1) splits = 1;
-    int kps = ((chunks + splits - 1) / splits) * 32;
+    int kps = ((chunks + splits - 1) / splits) * KC;
     splits = (K + kps - 1) / kps;
     if ((int64_t)splits * stride > c->ws_floats) { splits = 1; kps = K; }
     dim3 grid(tiles_n, splits, zb);
-    hipLaunchKernelGGL(k_gemm_bf16<MT>, grid, dim3(256), 0, c->stream, (const uint16_t*)X,
-                       (const uint16_t*)W, c->ws, M_ptr, N, K, kps, stride);
+    const uint16_t* Xh = (const uint16_t*)X;
+    const uint16_t* Wh = (const uint16_t*)W;
+#define SARA_GEMM(NT_, KC_) \
+    hipLaunchKernelGGL((k_gemm_bf16_lds<NT_, MT, KC_, 0>), grid, dim3(256), 0, c->stream, Xh, Wh, \
+                       (void*)c->ws, M_ptr, N, K, kps, stride)
+    if (wide) SARA_GEMM(2, 64);
+    else SARA_GEMM(1, 64);
+#undef SARA_GEMM
     splits_out = splits;
   } else {
     int tiles_n = (N + 15) / 16, zb = (M_cap + 15) / 16;
@@ -649,6 +920,16 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
 #define PROF_B(c) do { if ((c)->prof_active) prof_begin(c); } while (0)
 #define PROF_E(c, cls, N, K) do { if ((c)->prof_active) prof_end((c), (cls), (N), (K)); } while (0)
 
+// gate|up GEMM with the SwiGLU epilogue (bf16 models; W_gu rows interleaved
+// per 16-row tile at init), writing a = silu(g) * u to c->xa as [m][ffn]
+static void gemm_swiglu(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr, int M_cap) {
+  constexpr int MT = 8;
+  const int N = 2 * c->ffn, K = c->d;
+  dim3 grid((N + 127) / 128, 1, (M_cap + 16 * MT - 1) / (16 * MT));
+  hipLaunchKernelGGL((k_gemm_bf16_lds<2, MT, 64, 1>), grid, dim3(256), 0, c->stream, (const uint16_t*)X,
+                     (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0);
+}
+
 template <typename T, int HD>
 static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_norm_out) {
   hipStream_t st = c->stream;
@@ -661,45 +942,62 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     gemm(c, x, c->w_qkv[l], M_ptr, M_cap, c->nqkv, d, sp);
     PROF_E(c, kPGemm, c->nqkv, d);
     PROF_B(c);
-    hipLaunchKernelGGL(k_qkv_epilogue<T>, dim3(M_cap), dim3(256), 0, st, M_ptr, c->rows, c->ws, sp,
+    hipLaunchKernelGGL(k_qkv_epilogue<T>, dim3(2048), dim3(c->hd / 2), 0, st, M_ptr,
+                       c->rows, c->ws, sp,
                        stride_qkv, c->rope, c->hq, c->hkv, c->hd, l, c->n_blocks, c->btab, c->MAXB,
                        c->PB, (T*)c->qbuf, (T*)c->kc, (T*)c->vc);
     PROF_E(c, kPQkv, c->nqkv, 0);
     PROF_B(c);
-    hipLaunchKernelGGL((k_attention<T, HD>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
-                       M_ptr, c->rows, (const T*)c->qbuf, (const T*)c->kc, (const T*)c->vc, c->btab,
-                       c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv, c->attn_splits_max,
-                       1.0f / sqrtf((float)HD), c->attn_part);
+    const bool mfma_attn = (c->md.dtype == SARA_BF16);
+    if (mfma_attn)
+      hipLaunchKernelGGL((k_attn_mfma<HD>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
+                         M_ptr, c->rows, (const uint16_t*)c->qbuf, (const uint16_t*)c->kc,
+                         (const uint16_t*)c->vc, c->btab, c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv,
+                         c->attn_splits_max, 1.0f / sqrtf((float)HD), c->attn_part);
+    else
+      hipLaunchKernelGGL((k_attention<T, HD>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
+                         M_ptr, c->rows, (const T*)c->qbuf, (const T*)c->kc, (const T*)c->vc, c->btab,
+                         c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv, c->attn_splits_max,
+                         1.0f / sqrtf((float)HD), c->attn_part);
     PROF_E(c, kPAttn, 0, 0);
     PROF_B(c);
-    hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(M_cap, c->hq), dim3(HD), 0, st, M_ptr, c->rows,
-                       c->attn_part, c->hq, c->hkv, c->attn_splits_max, x);
+    hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(1024), dim3(HD), 0, st, M_ptr, c->rows,
+                       c->attn_part, c->hq, c->hkv, c->attn_splits_max, mfma_attn ? 1 : 0, x);
     PROF_E(c, kPCombine, 0, 0);
     PROF_B(c);
     gemm(c, x, c->w_o[l], M_ptr, M_cap, d, c->qdim, sp);
     PROF_E(c, kPGemm, d, c->qdim);
     PROF_B(c);
-    hipLaunchKernelGGL(k_residual_norm<T>, dim3(M_cap), dim3(256), 0, st, M_ptr, c->ws, sp,
+    hipLaunchKernelGGL(k_residual_norm<T>, dim3(std::min(M_cap, 256)), dim3(1024), 0, st, M_ptr, c->ws, sp,
                        (int64_t)M_cap * d, d, c->h, c->norms + (size_t)(2 * l + 1) * d,
                        c->md.rms_eps, x);
     PROF_E(c, kPResNorm, d, 0);
-    PROF_B(c);
-    gemm(c, x, c->w_gu[l], M_ptr, M_cap, 2 * c->ffn, d, sp);
-    PROF_E(c, kPGemm, 2 * c->ffn, d);
-    PROF_B(c);
-    hipLaunchKernelGGL(k_swiglu<T>, dim3((c->ffn + 255) / 256, M_cap), dim3(256), 0, st, M_ptr, c->ws,
-                       sp, (int64_t)M_cap * 2 * c->ffn, c->ffn, x);
-    PROF_E(c, kPSwiglu, c->ffn, 0);
-    PROF_B(c);
-    gemm(c, x, c->w_d[l], M_ptr, M_cap, d, c->ffn, sp);
-    PROF_E(c, kPGemm, d, c->ffn);
+    if (c->md.dtype == SARA_BF16) {
+      PROF_B(c);
+      gemm_swiglu(c, x, c->w_gu[l], M_ptr, M_cap);
+      PROF_E(c, kPGemm, 2 * c->ffn, d);
+      PROF_B(c);
+      gemm(c, c->xa, c->w_d[l], M_ptr, M_cap, d, c->ffn, sp);
+      PROF_E(c, kPGemm, d, c->ffn);
+    } else {
+      PROF_B(c);
+      gemm(c, x, c->w_gu[l], M_ptr, M_cap, 2 * c->ffn, d, sp);
+      PROF_E(c, kPGemm, 2 * c->ffn, d);
+      PROF_B(c);
+      hipLaunchKernelGGL(k_swiglu<T>, dim3(1024), dim3(256), 0, st, M_ptr, c->ws,
+                         sp, (int64_t)M_cap * 2 * c->ffn, c->ffn, x);
+      PROF_E(c, kPSwiglu, c->ffn, 0);
+      PROF_B(c);
+      gemm(c, x, c->w_d[l], M_ptr, M_cap, d, c->ffn, sp);
+      PROF_E(c, kPGemm, d, c->ffn);
+    }
     const float* nw = (l + 1 < c->L) ? c->norms + (size_t)(2 * (l + 1)) * d
                                      : c->norms + (size_t)(2 * c->L) * d;
     // the last layer's norm output is only needed when logits follow
     if (l + 1 < c->L || final_norm_out) {
       PROF_B(c);
-      hipLaunchKernelGGL(k_residual_norm<T>, dim3(M_cap), dim3(256), 0, st, M_ptr, c->ws, sp,
-                         (int64_t)M_cap * d, d, c->h, nw, c->md.rms_eps, x);
+      hipLaunchKernelGGL(k_residual_norm<T>, dim3(std::min(M_cap, 256)), dim3(1024), 0, st, M_ptr, c->ws,
+                         sp, (int64_t)M_cap * d, d, c->h, nw, c->md.rms_eps, x);
       PROF_E(c, kPResNorm, d, 0);
     }
   }
@@ -806,6 +1104,25 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
   (void)hipFreeAsync(mdev, st);
   e = hipStreamSynchronize(st);
   if (e != hipSuccess) return hip_fail(e, "sample_rows");
+  return SARA_OK;
+}
+
+// W_gu for the SwiGLU epilogue: 16-row tile 2j = gate rows [16j, 16j+16),
+// tile 2j+1 = up rows [16j, 16j+16)
+__global__ void k_interleave_gate_up(const uint16_t* __restrict__ wg, const uint16_t* __restrict__ wu,
+                                     uint16_t* __restrict__ dst, int ffn, int d) {
+  const size_t total = (size_t)2 * ffn * d;
+  for (size_t e = (size_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (size_t)gridDim.x * 256) {
+    size_t r = e / d, col = e - r * d;
+    size_t tile = r >> 4, within = r & 15;
+    size_t src_row = (tile >> 1) * 16 + within;
+    dst[e] = (tile & 1) ? wu[src_row * d + col] : wg[src_row * d + col];
+  }
+}
+
+int launch_interleave_gate_up(sara_ctx* c, const void* wg, const void* wu, void* dst) {
+  hipLaunchKernelGGL(k_interleave_gate_up, dim3(2048), dim3(256), 0, c->stream, (const uint16_t*)wg,
+                     (const uint16_t*)wu, (uint16_t*)dst, c->ffn, c->d);
   return SARA_OK;
 }
 

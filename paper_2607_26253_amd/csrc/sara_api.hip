@@ -36,7 +36,8 @@ static int einval(const std::string& msg) {
 const char* const kProfNames[kPNumClasses] = {
     "k_gemm_bf16 (decode GEMMs)", "k_attention", "k_attn_combine", "k_qkv_epilogue",
     "k_residual_norm", "k_swiglu", "k_embed_norm", "k_sample_partial", "k_sample_final",
-    "k_decode_rows", "k_copy_logits"};
+    "k_decode_rows", "k_copy_logits", ".gemm[q|k|v]", ".gemm[o]", ".gemm[gate|up]", ".gemm[down]",
+    ".gemm[lm_head]"};
 
 void prof_begin(sara_ctx* c) {
   if (c->prof_next_event + 2 > (int)c->prof_events.size()) return;
@@ -85,11 +86,21 @@ int prof_collect(sara_ctx* c) {
       case kPCopy: by = m * N * 8.0; break;
       default: by = m * 64.0; break;
     }
-    auto& t = c->prof_tot[r.cls];
-    t.launches += 1;
-    t.ms += ms;
-    t.bytes += by;
-    t.flops += fl;
+    auto add = [&](int cls) {
+      auto& t = c->prof_tot[cls];
+      t.launches += 1;
+      t.ms += ms;
+      t.bytes += by;
+      t.flops += fl;
+    };
+    add(r.cls);
+    if (r.cls == kPGemm) {
+      if (r.N == c->V) add(kPGemmLm);
+      else if (r.N == c->nqkv) add(kPGemmQkv);
+      else if (r.N == 2 * c->ffn) add(kPGemmGu);
+      else if (r.K == c->ffn) add(kPGemmD);
+      else add(kPGemmO);
+    }
   }
   c->prof_recs.clear();
   c->prof_next_event = 0;
@@ -131,8 +142,9 @@ static int validate(const sara_model_desc* m, const sara_alloc_desc* a) {
   if (m->n_kv_heads < 1 || m->n_heads % m->n_kv_heads != 0 ||
       m->n_heads / m->n_kv_heads > kMaxGroup)
     return einval("n_heads must be a multiple of n_kv_heads with at most 8 query heads per KV head");
-  if (m->d_model % 32 || m->d_ffn % 32 || (m->n_heads * m->head_dim) % 32)
-    return einval("d_model, d_ffn and n_heads*head_dim must be multiples of 32");
+  if (m->d_model % 64 || m->d_ffn % 64 || (m->n_heads * m->head_dim) % 64)
+    return einval("d_model, d_ffn and n_heads*head_dim must be multiples of 64");
+  if (m->dtype == SARA_BF16 && m->d_ffn % 16) return einval("d_ffn must be a multiple of 16");
   if (m->vocab % 16) return einval("vocab must be a multiple of 16");
   if (m->eos_id < -1 || m->eos_id >= m->vocab) return einval("eos_id out of range");
   if (!(m->rms_eps > 0.f) || !(m->rope_theta > 0.f)) return einval("rms_eps and rope_theta must be > 0");
@@ -189,7 +201,8 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   c->elt = (md->dtype == SARA_BF16) ? 2 : 4;
   c->prefill_rows = 4096;
   c->row_cap = std::max(c->S, c->prefill_rows);
-  c->attn_splits_max = (c->max_pos + kAttnSplit - 1) / kAttnSplit;
+  c->attn_splits_max = std::max((c->max_pos + kAttnSplit - 1) / kAttnSplit,
+                                (c->MAXB + kAttnChunks - 1) / kAttnChunks);
   {
     int64_t nd = std::max<int64_t>({c->V, c->nqkv, 2 * (int64_t)c->ffn, c->d});
     int64_t np = std::max<int64_t>({c->nqkv, 2 * (int64_t)c->ffn, c->d});
@@ -258,6 +271,7 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   ALLOC(c->h, sizeof(float) * (size_t)c->row_cap * d);
   ALLOC(c->x, (size_t)c->row_cap * std::max({c->d, c->ffn, c->qdim}) * E);
   ALLOC(c->qbuf, (size_t)c->row_cap * c->qdim * E);
+  ALLOC(c->xa, (size_t)c->row_cap * c->ffn * E);
   ALLOC(c->ws, sizeof(float) * (size_t)c->ws_floats);
   ALLOC(c->attn_part, sizeof(float) * (size_t)c->row_cap * c->hkv * c->attn_splits_max * kMaxGroup *
                           (c->hd + 2));
@@ -290,8 +304,13 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
     if (e == hipSuccess) e = cp(qkv + qb + kvb, w[3], kvb);
     if (e == hipSuccess) e = cp(c->w_o[l], w[4], (size_t)d * c->qdim * E);
     char* gu = (char*)c->w_gu[l];
-    if (e == hipSuccess) e = cp(gu, w[6], fb);
-    if (e == hipSuccess) e = cp(gu + fb, w[7], fb);
+    if (md->dtype == SARA_BF16) {
+      // tile-interleaved gate|up rows for the fused SwiGLU epilogue
+      if (e == hipSuccess) launch_interleave_gate_up(c, w[6], w[7], gu);
+    } else {
+      if (e == hipSuccess) e = cp(gu, w[6], fb);
+      if (e == hipSuccess) e = cp(gu + fb, w[7], fb);
+    }
     if (e == hipSuccess) e = cp(c->w_d[l], w[8], (size_t)d * c->ffn * E);
   }
   if (e == hipSuccess) e = cp(c->lm_head, d_weights[2 + 9 * c->L], (size_t)c->V * d * E);

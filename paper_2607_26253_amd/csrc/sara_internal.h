@@ -15,7 +15,8 @@ namespace sara {
 // constants
 // ---------------------------------------------------------------------------
 constexpr int kBlockTok = 16;        // KV page size in tokens
-constexpr int kAttnSplit = 512;      // tokens per attention context split
+constexpr int kAttnSplit = 256;      // tokens per context split (fp32 VALU attention)
+constexpr int kAttnChunks = 16;      // KV pages per context split (bf16 MFMA attention)
 constexpr int kAttnTile = 64;        // tokens per LDS tile inside a split
 constexpr int kSampleChunks = 16;    // vocabulary chunks per sampled row
 constexpr int kCtlThreads = 1024;    // threads of the single-workgroup controller
@@ -119,6 +120,7 @@ struct sara_ctx {
   float* h = nullptr;             // [row_cap][d] residual stream
   void* x = nullptr;              // [row_cap][max(d, ffn, qdim)] GEMM input (model dtype)
   void* qbuf = nullptr;           // [row_cap][hq][hd]
+  void* xa = nullptr;             // [row_cap][ffn] SwiGLU output (bf16 models)
   float* ws = nullptr;            // GEMM partial outputs
   float* attn_part = nullptr;
   float* samp_best = nullptr;
@@ -156,7 +158,9 @@ struct sara_ctx {
 namespace sara {
 
 enum ProfClass { kPGemm, kPAttn, kPCombine, kPQkv, kPResNorm, kPSwiglu, kPEmbed, kPSampleP,
-                 kPSampleF, kPRows, kPCopy, kPNumClasses };
+                 kPSampleF, kPRows, kPCopy,
+                 // breakdown of kPGemm by weight matrix (also counted in kPGemm)
+                 kPGemmQkv, kPGemmO, kPGemmGu, kPGemmD, kPGemmLm, kPNumClasses };
 extern const char* const kProfNames[kPNumClasses];
 void prof_begin(sara_ctx* c);
 void prof_end(sara_ctx* c, int cls, int N = 0, int K = 0);
@@ -181,6 +185,7 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
                        const int32_t* pos, uint64_t seed, int step, float temp, int eos,
                        uint32_t feos, int32_t* tok, hipStream_t st);
 int launch_convert_norms(sara_ctx* c, const void* const* w);
+int launch_interleave_gate_up(sara_ctx* c, const void* wg, const void* wu, void* dst);
 
 // ---------------------------------------------------------------------------
 // device helpers
