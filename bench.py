@@ -83,6 +83,9 @@ def main():
     ap.add_argument("--profile-every", type=int, default=16)
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-iters", type=int, default=0,
+                    help="profiling mode: only replay this many decode/decide/refill iterations of "
+                         "step 0 from the HIP graph (for kernel traces), then exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the allocation step is "
@@ -104,6 +107,23 @@ def main():
     del dw
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+    if args.decode_iters:
+        p = W.make_pool(cfg, 0)
+        d_tok, d_p = torch.from_numpy(p["tokens"]).cuda(), torch.from_numpy(p["p"]).cuda()
+        d_fl = torch.from_numpy(np.ascontiguousarray(p["forced_len"].reshape(-1))).cuda() \
+            if p["forced_len"] is not None else None
+        ctx.sara_begin_step(d_tok, p["offsets"], d_p, d_fl, p["step"])
+        ctx.sara_run(None, graph_iters=args.graph_iters, max_iters=args.graph_iters)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        n = ctx.sara_run(None, graph_iters=args.graph_iters, max_iters=args.decode_iters)
+        dt = time.perf_counter() - t0
+        q = ctx.sara_query()
+        print(json.dumps({"mode": "decode_iters", "workload": describe(cfg), "iters": n,
+                          "ms_per_iter": 1e3 * dt / n, "running_slots": q["running"], "tokens": q["tokens"]}))
+        ctx.close()
+        return
 
     n_total = args.warmup + args.steps + (0 if args.no_profile else 1)
     pools = []

@@ -52,29 +52,47 @@ __device__ float block_sum256(float v, float* red) {
 // ---------------------------------------------------------------------------
 // embedding gather + first RMSNorm (decode and prefill rows)
 // ---------------------------------------------------------------------------
-// Decode rows: row i of the batch is occupied slot active[i].
-__global__ __launch_bounds__(256) void k_decode_rows(const Ctl* __restrict__ ctl,
+// Decode rows + embedding gather + first RMSNorm in one launch: row i of the
+// batch is occupied slot active[i]; the device row count goes to rows_M.
+template <typename T>
+__global__ __launch_bounds__(256) void k_decode_embed(const Ctl* __restrict__ ctl,
     const int32_t* __restrict__ active, const int32_t* __restrict__ slot_uid,
     const int32_t* __restrict__ slot_j, const int32_t* __restrict__ slot_gen,
     const int32_t* __restrict__ tok, const int32_t* __restrict__ off,
-    const int32_t* __restrict__ out_tok, int k, int max_new, RowDesc* __restrict__ rows) {
-  int M = ctl->done ? 0 : ctl->M;
-  int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= M) return;
-  int s = active[i];
-  int u = slot_uid[s], j = slot_j[s], g = slot_gen[s];
-  int P = off[u + 1] - off[u];
-  int rid = u * k + j;
-  RowDesc r;
-  r.tok = (g == 0) ? tok[off[u] + P - 1] : out_tok[(size_t)rid * max_new + g - 1];
-  r.pos = P - 1 + g;
-  r.plen = P - 1;
-  r.tab = s;
-  r.slot = s;
-  r.rid = rid;
-  r.gen = g;
-  r.uid = u;
-  rows[i] = r;
+    const int32_t* __restrict__ out_tok, int k, int max_new, RowDesc* __restrict__ rows,
+    int32_t* __restrict__ rows_M, int do_embed, const T* __restrict__ embed,
+    const float* __restrict__ w, int d, float eps, float* __restrict__ h, T* __restrict__ x) {
+  __shared__ float red[4];
+  const int M = ctl->done ? 0 : ctl->M;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *rows_M = M;
+  for (int i = blockIdx.x; i < M; i += gridDim.x) {
+    const int s = active[i];
+    const int u = slot_uid[s], j = slot_j[s], g = slot_gen[s];
+    const int P = off[u + 1] - off[u];
+    const int rid = u * k + j;
+    RowDesc r;
+    r.tok = (g == 0) ? tok[off[u] + P - 1] : out_tok[(size_t)rid * max_new + g - 1];
+    r.pos = P - 1 + g;
+    r.plen = P - 1;
+    r.tab = s;
+    r.slot = s;
+    r.rid = rid;
+    r.gen = g;
+    r.uid = u;
+    if (threadIdx.x == 0) rows[i] = r;
+    if (!do_embed) continue;
+    float ss = 0.f;
+    for (int cc = threadIdx.x; cc < d; cc += 256) {
+      float v = ld_f32(embed, (size_t)r.tok * d + cc);
+      h[(size_t)i * d + cc] = v;
+      ss += v * v;
+    }
+    float tot = block_sum256(ss, red);
+    float inv = 1.0f / sqrtf(tot / (float)d + eps);
+    for (int cc = threadIdx.x; cc < d; cc += 256)
+      st_f32(x, (size_t)i * d + cc, h[(size_t)i * d + cc] * inv * w[cc]);
+    __syncthreads();   // red[] is reused by the next row
+  }
 }
 
 // Prefill rows of the chunk [r0, r0 + n): global prompt-token row r maps to
@@ -140,7 +158,8 @@ __global__ __launch_bounds__(256) void k_embed_norm(const int32_t* __restrict__ 
 // EPI = 1: SwiGLU epilogue (one split only): the weight rows are interleaved
 //          per 16-row tile as gate (even tiles) and up (odd tiles) of the same
 //          16 features; out receives bf16 silu(g) * u as [m][N/2].
-template <int NT, int MT, int KC, int EPI>
+// PF only separates the prefill instances from the decode ones in profiles.
+template <int NT, int MT, int KC, int EPI, int PF>
 __global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __restrict__ X,
     const uint16_t* __restrict__ W, void* __restrict__ out, const int32_t* __restrict__ M_ptr,
     int N, int K, int kps, int64_t split_stride) {
@@ -549,18 +568,30 @@ __global__ __launch_bounds__(256) void k_attention(const int32_t* __restrict__ M
 //                 the A operand's layout, V^T pages give the B operand; P is
 //                 split into bf16 hi + lo parts, two MFMAs)
 // The 4 waves' (max, sum, O) are merged in LDS into one partial per split.
-template <int HD>
+//
+// FUSE = 1 (decode rows): the block also forms its q heads from the fused
+// q|k|v GEMM partials (split sum, RoPE, bf16) and, if its split holds the
+// row's newest position, appends that position's k and v to the KV page
+// before reading it.  A row whose context fits one split writes its
+// normalised output straight to `out` ([row][hq][HD], bf16); other rows are
+// merged by the combine kernel.  (Merging in-kernel by the last-arriving
+// block would need a device-scope fence per block, which on this multi-XCD
+// part writes back the L2 and costs far more than a launch.)
+template <int HD, int FUSE>
 __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M_ptr,
     const RowDesc* __restrict__ rows, const uint16_t* __restrict__ qbuf,
-    const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+    uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
     const int32_t* __restrict__ btab, int MAXB, int PB, int layer, int64_t n_blocks, int hq,
-    int hkv, int n_splits, float scale, float* __restrict__ part) {
+    int hkv, int n_splits, float scale, float* __restrict__ part,
+    const float* __restrict__ qkv_ws, int qkv_splits, int64_t qkv_stride,
+    const float2* __restrict__ rope, uint16_t* __restrict__ out) {
   typedef short short4_ __attribute__((ext_vector_type(4)));
   constexpr int DPL = HD / 4;     // dims per lane in the QK^T operands
   constexpr int NCC = HD / 32;    // 16x16x32 MFMAs per page for QK^T
   constexpr int NT = HD / 16;     // output tiles of 16 dims
   __shared__ float m_w[4][16], l_w[4][16];
   __shared__ float o_w[4][16][HD + 1];
+  __shared__ __attribute__((aligned(16))) uint16_t q_s[kMaxGroup][HD];
   const int i = blockIdx.x, g = blockIdx.y, c = blockIdx.z;
   if (i >= *M_ptr) return;
   const RowDesc r = rows[i];
@@ -575,10 +606,42 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
   const int G = hq / hkv;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = lane & 15, grp = lane >> 4;
+  const int half = HD / 2;
+  if (FUSE) {
+    // q heads of this group, and (last split only) this position's k and v
+    const int nqkv = (hq + 2 * hkv) * HD;
+    const size_t rb = (size_t)i * nqkv;
+    for (int e = threadIdx.x; e < G * half; e += 256) {
+      int gh = e / half, cc = e - gh * half;
+      size_t col = (size_t)(g * G + gh) * HD + cc;
+      float a = split_sum(qkv_ws, qkv_splits, qkv_stride, rb + col);
+      float b = split_sum(qkv_ws, qkv_splits, qkv_stride, rb + col + half);
+      float2 cs = rope[(size_t)r.pos * half + cc];
+      q_s[gh][cc] = f32_to_bf16(a * cs.x - b * cs.y);
+      q_s[gh][cc + half] = f32_to_bf16(b * cs.x + a * cs.y);
+    }
+    if (ch1 == nch && threadIdx.x < HD) {
+      const int cc = threadIdx.x;
+      if (cc < half) {
+        size_t col = (size_t)(hq + g) * HD + cc;
+        float a = split_sum(qkv_ws, qkv_splits, qkv_stride, rb + col);
+        float b = split_sum(qkv_ws, qkv_splits, qkv_stride, rb + col + half);
+        float2 cs = rope[(size_t)r.pos * half + cc];
+        kc[kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc, r.pos)] = f32_to_bf16(a * cs.x - b * cs.y);
+        kc[kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc + half, r.pos)] =
+            f32_to_bf16(b * cs.x + a * cs.y);
+      }
+      size_t colv = (size_t)(hq + hkv + g) * HD + cc;
+      vc[vt_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc, r.pos)] =
+          f32_to_bf16(split_sum(qkv_ws, qkv_splits, qkv_stride, rb + colv));
+    }
+    __syncthreads();
+  }
   // q operand: head `row` of this KV group (zero beyond G), dims [DPL*grp, DPL*grp + DPL)
   uint4 qv[NCC];
   if (row < G) {
-    const uint4* qp = (const uint4*)(qbuf + ((size_t)i * hq + g * G + row) * HD + DPL * grp);
+    const uint4* qp = FUSE ? (const uint4*)(&q_s[row][DPL * grp])
+                           : (const uint4*)(qbuf + ((size_t)i * hq + g * G + row) * HD + DPL * grp);
 #pragma unroll
     for (int cc = 0; cc < NCC; ++cc) qv[cc] = qp[cc];
   } else {
@@ -662,6 +725,7 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
 #pragma unroll
     for (int q = 0; q < 4; ++q) o_w[wave][4 * grp + q][16 * t + row] = o[t][q];
   __syncthreads();
+  const int ns = (nch + kAttnChunks - 1) / kAttnChunks;
   for (int e = threadIdx.x; e < G * HD; e += 256) {
     int h = e / HD, dd = e - h * HD;
     float mx = fmaxf(fmaxf(m_w[0][h], m_w[1][h]), fmaxf(m_w[2][h], m_w[3][h]));
@@ -672,17 +736,22 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
       num += wt * o_w[w][h][dd];
       den += wt * l_w[w][h];
     }
-    float* dst = part + ((((size_t)i * hkv + g) * n_splits + c) * kMaxGroup + h) * (HD + 2);
-    dst[dd] = num;
-    if (dd == 0) { dst[HD] = mx; dst[HD + 1] = den; }
+    if (FUSE && ns == 1) {
+      out[((size_t)i * hq + g * G + h) * HD + dd] = f32_to_bf16(num / den);
+    } else {
+      float* dst = part + ((((size_t)i * hkv + g) * n_splits + c) * kMaxGroup + h) * (HD + 2);
+      dst[dd] = num;
+      if (dd == 0) { dst[HD] = mx; dst[HD + 1] = den; }
+    }
   }
 }
 
 // merge the context splits of every (row, query head) into o (model dtype)
+// skip_single: rows with one split were written by the attention kernel.
 template <typename T, int HD>
 __global__ __launch_bounds__(HD) void k_attn_combine(const int32_t* __restrict__ M_ptr,
     const RowDesc* __restrict__ rows, const float* __restrict__ part, int hq, int hkv,
-    int n_splits, int paged_splits, T* __restrict__ out) {
+    int n_splits, int paged_splits, int skip_single, T* __restrict__ out) {
   const int M = *M_ptr;
   for (int item = blockIdx.x; item < M * hq; item += gridDim.x) {
   const int i = item / hq, h = item - i * hq;
@@ -697,6 +766,7 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const int32_t* __restrict__
   } else {
     ns = (ctx + kAttnSplit - 1) / kAttnSplit;
   }
+  if (skip_single && ns == 1) continue;
   const float* base = part + (((size_t)i * hkv + g) * n_splits * kMaxGroup + gh) * (HD + 2);
   const size_t sstride = (size_t)kMaxGroup * (HD + 2);
   float mx = -INFINITY;
@@ -858,10 +928,6 @@ __global__ void k_copy_logits(const Ctl* __restrict__ ctl, const RowDesc* __rest
     dst[(size_t)s * V + v] = ws[(size_t)i * V + v];
 }
 
-// M of the decode batch as a plain device int for the shared kernels
-__global__ void k_decode_M(const Ctl* __restrict__ ctl, int32_t* __restrict__ M_out) {
-  *M_out = ctl->done ? 0 : ctl->M;
-}
 
 // ---------------------------------------------------------------------------
 // host launchers
@@ -892,11 +958,16 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     dim3 grid(tiles_n, splits, zb);
     const uint16_t* Xh = (const uint16_t*)X;
     const uint16_t* Wh = (const uint16_t*)W;
-#define SARA_GEMM(NT_, KC_) \
-    hipLaunchKernelGGL((k_gemm_bf16_lds<NT_, MT, KC_, 0>), grid, dim3(256), 0, c->stream, Xh, Wh, \
+#define SARA_GEMM(NT_, KC_, PF_) \
+    hipLaunchKernelGGL((k_gemm_bf16_lds<NT_, MT, KC_, 0, PF_>), grid, dim3(256), 0, c->stream, Xh, Wh, \
                        (void*)c->ws, M_ptr, N, K, kps, stride)
-    if (wide) SARA_GEMM(2, 64);
-    else SARA_GEMM(1, 64);
+    if (c->in_prefill) {
+      if (wide) SARA_GEMM(2, 64, 1);
+      else SARA_GEMM(1, 64, 1);
+    } else {
+      if (wide) SARA_GEMM(2, 64, 0);
+      else SARA_GEMM(1, 64, 0);
+    }
 #undef SARA_GEMM
     splits_out = splits;
   } else {
@@ -926,8 +997,12 @@ static void gemm_swiglu(sara_ctx* c, const void* X, const void* W, const int32_t
   constexpr int MT = 8;
   const int N = 2 * c->ffn, K = c->d;
   dim3 grid((N + 127) / 128, 1, (M_cap + 16 * MT - 1) / (16 * MT));
-  hipLaunchKernelGGL((k_gemm_bf16_lds<2, MT, 64, 1>), grid, dim3(256), 0, c->stream, (const uint16_t*)X,
-                     (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0);
+  if (c->in_prefill)
+    hipLaunchKernelGGL((k_gemm_bf16_lds<2, MT, 64, 1, 1>), grid, dim3(256), 0, c->stream, (const uint16_t*)X,
+                       (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0);
+  else
+    hipLaunchKernelGGL((k_gemm_bf16_lds<2, MT, 64, 1, 0>), grid, dim3(256), 0, c->stream, (const uint16_t*)X,
+                       (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0);
 }
 
 template <typename T, int HD>
@@ -940,7 +1015,22 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     int sp;
     PROF_B(c);
     gemm(c, x, c->w_qkv[l], M_ptr, M_cap, c->nqkv, d, sp);
-    PROF_E(c, kPGemm, c->nqkv, d);
+    PROF_E(c, kPGemmN1, c->nqkv, d);
+    const bool mfma_attn = (c->md.dtype == SARA_BF16);
+    if (mfma_attn && !c->in_prefill) {
+      // decode: q|k|v epilogue, attention and split merge in one kernel
+      PROF_B(c);
+      hipLaunchKernelGGL((k_attn_mfma<HD, 1>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
+                         M_ptr, c->rows, (const uint16_t*)c->qbuf, (uint16_t*)c->kc, (uint16_t*)c->vc, c->btab,
+                         c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv, c->attn_splits_max,
+                         1.0f / sqrtf((float)HD), c->attn_part, (const float*)c->ws, sp, stride_qkv, c->rope,
+                         (uint16_t*)x);
+      PROF_E(c, kPAttn, 0, 0);
+      PROF_B(c);
+      hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(1024), dim3(HD), 0, st, M_ptr, c->rows,
+                         c->attn_part, c->hq, c->hkv, c->attn_splits_max, 1, 1, x);
+      PROF_E(c, kPCombine, 0, 0);
+    } else {
     PROF_B(c);
     hipLaunchKernelGGL(k_qkv_epilogue<T>, dim3(2048), dim3(c->hd / 2), 0, st, M_ptr,
                        c->rows, c->ws, sp,
@@ -948,12 +1038,12 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
                        c->PB, (T*)c->qbuf, (T*)c->kc, (T*)c->vc);
     PROF_E(c, kPQkv, c->nqkv, 0);
     PROF_B(c);
-    const bool mfma_attn = (c->md.dtype == SARA_BF16);
     if (mfma_attn)
-      hipLaunchKernelGGL((k_attn_mfma<HD>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
-                         M_ptr, c->rows, (const uint16_t*)c->qbuf, (const uint16_t*)c->kc,
-                         (const uint16_t*)c->vc, c->btab, c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv,
-                         c->attn_splits_max, 1.0f / sqrtf((float)HD), c->attn_part);
+      hipLaunchKernelGGL((k_attn_mfma<HD, 0>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
+                         M_ptr, c->rows, (const uint16_t*)c->qbuf, (uint16_t*)c->kc,
+                         (uint16_t*)c->vc, c->btab, c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv,
+                         c->attn_splits_max, 1.0f / sqrtf((float)HD), c->attn_part, (const float*)nullptr, 0,
+                         (int64_t)0, c->rope, (uint16_t*)nullptr);
     else
       hipLaunchKernelGGL((k_attention<T, HD>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
                          M_ptr, c->rows, (const T*)c->qbuf, (const T*)c->kc, (const T*)c->vc, c->btab,
@@ -962,11 +1052,12 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     PROF_E(c, kPAttn, 0, 0);
     PROF_B(c);
     hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(1024), dim3(HD), 0, st, M_ptr, c->rows,
-                       c->attn_part, c->hq, c->hkv, c->attn_splits_max, mfma_attn ? 1 : 0, x);
+                       c->attn_part, c->hq, c->hkv, c->attn_splits_max, mfma_attn ? 1 : 0, 0, x);
     PROF_E(c, kPCombine, 0, 0);
+    }
     PROF_B(c);
     gemm(c, x, c->w_o[l], M_ptr, M_cap, d, c->qdim, sp);
-    PROF_E(c, kPGemm, d, c->qdim);
+    PROF_E(c, kPGemmN1, d, c->qdim);
     PROF_B(c);
     hipLaunchKernelGGL(k_residual_norm<T>, dim3(std::min(M_cap, 256)), dim3(1024), 0, st, M_ptr, c->ws, sp,
                        (int64_t)M_cap * d, d, c->h, c->norms + (size_t)(2 * l + 1) * d,
@@ -975,21 +1066,21 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     if (c->md.dtype == SARA_BF16) {
       PROF_B(c);
       gemm_swiglu(c, x, c->w_gu[l], M_ptr, M_cap);
-      PROF_E(c, kPGemm, 2 * c->ffn, d);
+      PROF_E(c, kPGemmGU, 2 * c->ffn, d);
       PROF_B(c);
       gemm(c, c->xa, c->w_d[l], M_ptr, M_cap, d, c->ffn, sp);
-      PROF_E(c, kPGemm, d, c->ffn);
+      PROF_E(c, kPGemmN1, d, c->ffn);
     } else {
       PROF_B(c);
       gemm(c, x, c->w_gu[l], M_ptr, M_cap, 2 * c->ffn, d, sp);
-      PROF_E(c, kPGemm, 2 * c->ffn, d);
+      PROF_E(c, kPGemmN1, 2 * c->ffn, d);
       PROF_B(c);
       hipLaunchKernelGGL(k_swiglu<T>, dim3(1024), dim3(256), 0, st, M_ptr, c->ws,
                          sp, (int64_t)M_cap * 2 * c->ffn, c->ffn, x);
       PROF_E(c, kPSwiglu, c->ffn, 0);
       PROF_B(c);
       gemm(c, x, c->w_d[l], M_ptr, M_cap, d, c->ffn, sp);
-      PROF_E(c, kPGemm, d, c->ffn);
+      PROF_E(c, kPGemmN1, d, c->ffn);
     }
     const float* nw = (l + 1 < c->L) ? c->norms + (size_t)(2 * (l + 1)) * d
                                      : c->norms + (size_t)(2 * c->L) * d;
@@ -1011,6 +1102,7 @@ static void layers(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_norm
 
 int launch_prefill(sara_ctx* c) {
   hipStream_t st = c->stream;
+  c->in_prefill = true;
   // prefix sums of (P - 1): prompt-token rows of the pool, chunked
   std::vector<int64_t> pre(c->U + 1, 0);
   for (int u = 0; u < c->U; ++u) pre[u + 1] = pre[u] + (c->h_off[u + 1] - c->h_off[u] - 1);
@@ -1030,6 +1122,7 @@ int launch_prefill(sara_ctx* c) {
       layers<float>(c, c->rows_M, n, false);
     }
   }
+  c->in_prefill = false;
   return SARA_OK;
 }
 
@@ -1037,28 +1130,26 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
   hipStream_t st = c->stream;
   const int S = c->S;
   PROF_B(c);
-  hipLaunchKernelGGL(k_decode_M, dim3(1), dim3(1), 0, st, c->ctl, c->rows_M);
-  hipLaunchKernelGGL(k_decode_rows, dim3((S + 255) / 256), dim3(256), 0, st, c->ctl, c->active,
-                     c->slot_uid, c->slot_j, c->slot_gen, c->tok, c->off, c->out_tok, c->k,
-                     c->ad.max_new, c->rows);
-  PROF_E(c, kPRows, 0, 0);
+  const int eg = std::min(S, 512);
+  if (c->md.dtype == SARA_BF16)
+    hipLaunchKernelGGL(k_decode_embed<uint16_t>, dim3(eg), dim3(256), 0, st, c->ctl, c->active, c->slot_uid,
+                       c->slot_j, c->slot_gen, c->tok, c->off, c->out_tok, c->k, c->ad.max_new, c->rows,
+                       c->rows_M, model_free ? 0 : 1, (const uint16_t*)c->embed, c->norms, c->d,
+                       c->md.rms_eps, c->h, (uint16_t*)c->x);
+  else
+    hipLaunchKernelGGL(k_decode_embed<float>, dim3(eg), dim3(256), 0, st, c->ctl, c->active, c->slot_uid,
+                       c->slot_j, c->slot_gen, c->tok, c->off, c->out_tok, c->k, c->ad.max_new, c->rows,
+                       c->rows_M, model_free ? 0 : 1, (const float*)c->embed, c->norms, c->d,
+                       c->md.rms_eps, c->h, (float*)c->x);
+  PROF_E(c, kPEmbed, c->d, 0);
   if (!model_free) {
-    PROF_B(c);
-    if (c->md.dtype == SARA_BF16)
-      hipLaunchKernelGGL(k_embed_norm<uint16_t>, dim3(S), dim3(256), 0, st, c->rows_M, c->rows,
-                         (const uint16_t*)c->embed, c->norms, c->d, c->md.rms_eps, c->h,
-                         (uint16_t*)c->x);
-    else
-      hipLaunchKernelGGL(k_embed_norm<float>, dim3(S), dim3(256), 0, st, c->rows_M, c->rows,
-                         (const float*)c->embed, c->norms, c->d, c->md.rms_eps, c->h, (float*)c->x);
-    PROF_E(c, kPEmbed, c->d, 0);
     if (c->md.dtype == SARA_BF16) layers<uint16_t>(c, c->rows_M, S, true);
     else layers<float>(c, c->rows_M, S, true);
     int sp;
     // one K split: ws then holds the logits [M][V] directly
     PROF_B(c);
     gemm(c, c->x, c->lm_head, c->rows_M, S, c->V, c->d, sp, 1);
-    PROF_E(c, kPGemm, c->V, c->d);
+    PROF_E(c, kPGemmLM, c->V, c->d);
     PROF_B(c);
     hipLaunchKernelGGL(k_sample_partial, dim3(S, kSampleChunks), dim3(256), 0, st, c->rows_M,
                        (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, c->ws, c->V,

@@ -34,10 +34,10 @@ static int einval(const std::string& msg) {
 }
 
 const char* const kProfNames[kPNumClasses] = {
-    "k_gemm_bf16 (decode GEMMs)", "k_attention", "k_attn_combine", "k_qkv_epilogue",
-    "k_residual_norm", "k_swiglu", "k_embed_norm", "k_sample_partial", "k_sample_final",
-    "k_decode_rows", "k_copy_logits", ".gemm[q|k|v]", ".gemm[o]", ".gemm[gate|up]", ".gemm[down]",
-    ".gemm[lm_head]"};
+    "k_gemm_bf16_lds<1,8,64,0,0>", "k_gemm_bf16_lds<2,8,64,1,0>", "k_gemm_bf16_lds<2,8,64,0,0>",
+    "k_attn_mfma<128>", "k_attn_combine", "k_qkv_epilogue", "k_residual_norm", "k_swiglu",
+    "k_embed_norm", "k_sample_partial", "k_sample_final", "k_decode_rows", "k_copy_logits",
+    ".gemm[q|k|v]", ".gemm[o]", ".gemm[gate|up]", ".gemm[down]", ".gemm[lm_head]"};
 
 void prof_begin(sara_ctx* c) {
   if (c->prof_next_event + 2 > (int)c->prof_events.size()) return;
@@ -72,7 +72,10 @@ int prof_collect(sara_ctx* c) {
     HIP_TRY(hipEventElapsedTime(&ms, c->prof_events[r.e0], c->prof_events[r.e1]), "elapsed");
     double by = 0.0, fl = 0.0, N = r.N, K = r.K;
     switch (r.cls) {
-      case kPGemm: by = N * K * E + m * K * E + m * N * 4.0; fl = 2.0 * m * N * K; break;
+      case kPGemmN1: case kPGemmLM:
+        by = N * K * E + m * K * E + m * N * 4.0; fl = 2.0 * m * N * K; break;
+      case kPGemmGU:   // output is the bf16 SwiGLU product [m][N/2]
+        by = N * K * E + m * K * E + m * (N / 2) * E; fl = 2.0 * m * N * K; break;
       case kPAttn:
         by = sum_ctx * c->hkv * c->hd * E * 2.0 + m * c->qdim * E;
         fl = 4.0 * sum_ctx * c->qdim;
@@ -94,7 +97,7 @@ int prof_collect(sara_ctx* c) {
       t.flops += fl;
     };
     add(r.cls);
-    if (r.cls == kPGemm) {
+    if (r.cls == kPGemmN1 || r.cls == kPGemmGU || r.cls == kPGemmLM) {
       if (r.N == c->V) add(kPGemmLm);
       else if (r.N == c->nqkv) add(kPGemmQkv);
       else if (r.N == 2 * c->ffn) add(kPGemmGu);

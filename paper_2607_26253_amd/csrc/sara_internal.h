@@ -145,6 +145,7 @@ struct sara_ctx {
   bool prof_enabled = false;
   bool prof_active = false;
   bool capturing = false;
+  bool in_prefill = false;
   std::vector<hipEvent_t> prof_events;
   std::vector<ProfRec> prof_recs;
   int prof_next_event = 0;
@@ -157,9 +158,10 @@ struct sara_ctx {
 
 namespace sara {
 
-enum ProfClass { kPGemm, kPAttn, kPCombine, kPQkv, kPResNorm, kPSwiglu, kPEmbed, kPSampleP,
-                 kPSampleF, kPRows, kPCopy,
-                 // breakdown of kPGemm by weight matrix (also counted in kPGemm)
+// one class per kernel (per template instance for the GEMMs, as a kernel
+// trace names them), then a breakdown of the GEMMs by weight matrix
+enum ProfClass { kPGemmN1, kPGemmGU, kPGemmLM, kPAttn, kPCombine, kPQkv, kPResNorm, kPSwiglu,
+                 kPEmbed, kPSampleP, kPSampleF, kPRows, kPCopy,
                  kPGemmQkv, kPGemmO, kPGemmGu, kPGemmD, kPGemmLm, kPNumClasses };
 extern const char* const kProfNames[kPNumClasses];
 void prof_begin(sara_ctx* c);
