@@ -56,19 +56,20 @@ def cpu_baseline(cfg, weights, seconds_target=15.0):
     for name, _ in W.weight_specs(c["model"]):   # weight conversion outside the timing
         src.dec.w(name)
     t_setup = time.time() - t0
-    rollouts, new_tokens = 2, 4
+    prompts, rollouts, new_tokens = 2, 4, 16
     a_max = a["max_new"]
     src.a = dict(a, max_new=new_tokens)
     t0 = time.time()
-    src._generate([(0, j) for j in range(rollouts)])
+    pairs = [(u, j) for u in range(prompts) for j in range(rollouts)]
+    src._generate(pairs)
     t_run = time.time() - t0
-    n_tok = sum(src.results[(0, j)]["length"] for j in range(rollouts))
-    P = int(pool["offsets"][1] - pool["offsets"][0])
+    n_tok = sum(src.results[pr]["length"] for pr in pairs)
+    P = [int(pool["offsets"][u + 1] - pool["offsets"][u]) for u in range(prompts)]
     src.a = dict(a, max_new=a_max)
     return dict(value=n_tok / t_run, unit="tokens/s", cores=int(threads), kind="oracle",
-                sample=(f"{cfg['name']} shape: prefill of one {P}-token prompt + {rollouts} rollouts x "
-                        f"{new_tokens} tokens (generated tokens / wall time incl. prefill; weight cache "
-                        f"warm-up {t_setup:.1f}s excluded)"),
+                sample=(f"{cfg['name']} shape: prefill of {prompts} prompts ({P} tokens) + {rollouts} rollouts "
+                        f"each x up to {new_tokens} tokens, lockstep ({n_tok} generated tokens / wall time incl. "
+                        f"prefill; weight conversion {t_setup:.1f}s excluded)"),
                 seconds=t_run)
 
 

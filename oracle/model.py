@@ -113,8 +113,9 @@ class Decoder:
                 for _ in range(self.L)]
 
     # -- forward over a set of new positions of ONE sequence --------------
-    def forward(self, tokens, positions, cache, want_logits=True):
-        """Append tokens at `positions` (consecutive) to `cache`, causal."""
+    def forward(self, tokens, positions, cache, want_logits=True, logit_rows=None):
+        """Append tokens at `positions` (consecutive) to `cache`, causal.
+        logit_rows: optional indices of the rows whose logits are returned."""
         tokens = np.asarray(tokens, dtype=np.int64)
         positions = np.asarray(positions, dtype=np.int64)
         T = len(tokens)
@@ -139,6 +140,8 @@ class Decoder:
             h = h + self.mm(a, f"l{l}.wd")
         if not want_logits:
             return None
+        if logit_rows is not None:
+            h = h[np.asarray(logit_rows)]
         x = self.rnd(self.rmsnorm(h, "final_norm"))
         return self.mm(x, "lm_head").astype(np.float32)
 

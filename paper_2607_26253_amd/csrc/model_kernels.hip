@@ -171,8 +171,9 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __rest
   constexpr int RING = 4;
   __shared__ __attribute__((aligned(16))) uint16_t xs[2][MR * PITCH];
   const int M = *M_ptr;
-  const int m_base = blockIdx.z * MR;
-  if (m_base >= M) return;
+  // m-blocks of 16*MT rows: one per grid z (prefill) or all of them in turn
+  // (decode launches with grid z = 1 since M lives on the device)
+  for (int m_base = blockIdx.z * MR; m_base < M; m_base += gridDim.z * MR) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = lane & 15, grp = lane >> 4;
   const int n0 = (blockIdx.x * 4 + wave) * 16 * NT;
@@ -278,6 +279,8 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __rest
         }
       }
     }
+  }
+  __syncthreads();   // the LDS tiles are reused by the next m-block
   }
 }
 
@@ -592,8 +595,13 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
   __shared__ float m_w[4][16], l_w[4][16];
   __shared__ float o_w[4][16][HD + 1];
   __shared__ __attribute__((aligned(16))) uint16_t q_s[kMaxGroup][HD];
-  const int i = blockIdx.x, g = blockIdx.y, c = blockIdx.z;
-  if (i >= *M_ptr) return;
+  // persistent over work items (split c, row i, KV head g), split-major, so
+  // that no block waits only to find its row absent
+  const int M = *M_ptr;
+  const int total = M * hkv * n_splits;
+  for (int item = blockIdx.x; item < total; item += gridDim.x) {
+  const int c = item / (M * hkv);
+  const int i = (item - c * M * hkv) / hkv, g = item % hkv;
   const RowDesc r = rows[i];
   const int ctx = r.pos + 1;
   const int pl = min(ctx, r.plen);                      // prompt positions attended
@@ -601,11 +609,106 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
   const int vcnt = ctx - pl;                             // private positions
   const int nch = pc + ((vcnt + 15) >> 4);
   const int ch0 = c * kAttnChunks;
-  if (ch0 >= nch) return;
+  if (ch0 >= nch) continue;
   const int ch1 = min(nch, ch0 + kAttnChunks);
   const int G = hq / hkv;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = lane & 15, grp = lane >> 4;
+  // per-wave softmax state and output accumulators; q operand (set below)
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 o[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint4 qv[NCC];
+  const int32_t* bt = btab + (size_t)r.tab * MAXB;
+  // Block-table entries of this split's pages, one per lane 0..15, shared by
+  // shuffles (no table load on the page path).
+  int my_blk = 0;
+  if (lane < kAttnChunks && ch0 + lane < ch1) {
+    const int cl = ch0 + lane;
+    my_blk = bt[(cl < pc) ? cl : PB + (cl - pc)];
+  }
+  // Two page slots per wave: the next page's K, V (and its valid count) are
+  // loaded while the current one is processed.  Loads past the wave's last
+  // page re-read its first page (always valid) and are never used.
+  typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+  struct Pg { u32x4 k[NCC]; u32x2 v[NT]; int n; };
+  auto load_page = [&](Pg& P, int ch) {
+    const int cv = (ch < ch1) ? ch : (ch0 + wave);
+    int n;
+    if (cv < pc) n = min(16, pl - 16 * cv);
+    else n = min(16, vcnt - 16 * (cv - pc));
+    P.n = (ch < ch1) ? n : 0;
+    const int blk = __shfl(my_blk, cv - ch0, 64);
+    const size_t pg = ((size_t)layer * n_blocks + blk) * hkv + g;
+    const u32x4* kp = (const u32x4*)(kc + (pg * kBlockTok + row) * HD + DPL * grp);
+#pragma unroll
+    for (int cc = 0; cc < NCC; ++cc) P.k[cc] = kp[cc];
+    const uint16_t* vp = vc + pg * (size_t)HD * kBlockTok + 4 * grp;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) P.v[t] = *(const u32x2*)(vp + (size_t)(16 * t + row) * kBlockTok);
+  };
+  auto process_page = [&](const Pg& P) {
+    const int n = P.n;
+    // S^T[token][head]
+    f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int cc = 0; cc < NCC; ++cc)
+      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, P.k[cc]),
+                                                   __builtin_bit_cast(bf16x8, qv[cc]), sc, 0, 0, 0);
+    // lane holds tokens 4*grp + q (q < 4) of head `row`
+    float sv[4];
+    float mt = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      sv[q] = (4 * grp + q < n) ? sc[q] * scale : -INFINITY;
+      mt = fmaxf(mt, sv[q]);
+    }
+    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    const float mn = fmaxf(m_run, mt);
+    const float alpha = expf(m_run - mn);
+    // P enters the MFMA as a bf16 pair hi + lo (|p - hi - lo| <= 2^-16 p), so
+    // the PV product keeps fp32 accuracy without a bf16 rounding point
+    float ps = 0.f;
+    uint16_t pb[4], plo[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float pv = expf(sv[q] - mn);
+      uint16_t bb = f32_to_bf16(pv);
+      pb[q] = bb;
+      plo[q] = f32_to_bf16(pv - bf16_to_f32(bb));
+      ps += pv;
+    }
+    ps += __shfl_xor(ps, 16, 64);
+    ps += __shfl_xor(ps, 32, 64);
+    l_run = l_run * alpha + ps;
+    m_run = mn;
+    // rows of O are heads 4*grp + q: fetch their rescale factors
+    float al[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) al[q] = __shfl(alpha, 4 * grp + q, 64);
+    short4_ pa, pa_lo;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) { pa[q] = (short)pb[q]; pa_lo[q] = (short)plo[q]; }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      // positions beyond the page's n valid tokens may hold stale bits: zero them
+      short4_ vb;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t w = (q < 2) ? P.v[t].x : P.v[t].y;
+        uint16_t h = (uint16_t)((q & 1) ? (w >> 16) : (w & 0xFFFF));
+        vb[q] = (short)((4 * grp + q < n) ? h : (uint16_t)0);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[t][q] *= al[q];
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, vb, o[t], 0, 0, 0);
+      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa_lo, vb, o[t], 0, 0, 0);
+    }
+  };
+  Pg pa_, pb_;
+  load_page(pa_, ch0 + wave);
   const int half = HD / 2;
   if (FUSE) {
     // q heads of this group, and (last split only) this position's k and v
@@ -637,8 +740,10 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
     }
     __syncthreads();
   }
+  // the newest position was appended after the early load of this wave's
+  // first page: reload that page if it is the one holding it
+  if (FUSE && ch1 == nch && ch0 + wave == nch - 1) load_page(pa_, ch0 + wave);
   // q operand: head `row` of this KV group (zero beyond G), dims [DPL*grp, DPL*grp + DPL)
-  uint4 qv[NCC];
   if (row < G) {
     const uint4* qp = FUSE ? (const uint4*)(&q_s[row][DPL * grp])
                            : (const uint4*)(qbuf + ((size_t)i * hq + g * G + row) * HD + DPL * grp);
@@ -648,75 +753,12 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
 #pragma unroll
     for (int cc = 0; cc < NCC; ++cc) qv[cc] = make_uint4(0, 0, 0, 0);
   }
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4 o[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int32_t* bt = btab + (size_t)r.tab * MAXB;
-  for (int ch = ch0 + wave; ch < ch1; ch += 4) {
-    int e, n;
-    if (ch < pc) { e = ch; n = min(16, pl - 16 * ch); }
-    else { int j = ch - pc; e = PB + j; n = min(16, vcnt - 16 * j); }
-    const size_t pg = ((size_t)layer * n_blocks + bt[e]) * hkv + g;
-    // S^T[token][head]
-    const uint4* kp = (const uint4*)(kc + (pg * kBlockTok + row) * HD + DPL * grp);
-    f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int cc = 0; cc < NCC; ++cc)
-      sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kp[cc]),
-                                                   __builtin_bit_cast(bf16x8, qv[cc]), sc, 0, 0, 0);
-    // lane holds tokens 4*grp + q (q < 4) of head `row`
-    float sv[4];
-    float mt = -INFINITY;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      sv[q] = (4 * grp + q < n) ? sc[q] * scale : -INFINITY;
-      mt = fmaxf(mt, sv[q]);
-    }
-    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float mn = fmaxf(m_run, mt);
-    const float alpha = expf(m_run - mn);
-    // P enters the MFMA as a bf16 pair hi + lo (|p - hi - lo| <= 2^-16 p), so
-    // the PV product keeps fp32 accuracy without a bf16 rounding point
-    float ps = 0.f;
-    uint16_t pb[4], pl[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      float pv = expf(sv[q] - mn);
-      uint16_t b = f32_to_bf16(pv);
-      pb[q] = b;
-      pl[q] = f32_to_bf16(pv - bf16_to_f32(b));
-      ps += pv;
-    }
-    ps += __shfl_xor(ps, 16, 64);
-    ps += __shfl_xor(ps, 32, 64);
-    l_run = l_run * alpha + ps;
-    m_run = mn;
-    // rows of O are heads 4*grp + q: fetch their rescale factors
-    float al[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) al[q] = __shfl(alpha, 4 * grp + q, 64);
-    short4_ pa, pa_lo;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) { pa[q] = (short)pb[q]; pa_lo[q] = (short)pl[q]; }
-    const uint16_t* vp = vc + pg * (size_t)HD * kBlockTok + 4 * grp;
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      uint2 vv = *(const uint2*)(vp + (size_t)(16 * t + row) * kBlockTok);
-      // positions beyond the page's n valid tokens may hold stale bits: zero them
-      short4_ vb;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        uint32_t w = (q < 2) ? vv.x : vv.y;
-        uint16_t h = (uint16_t)((q & 1) ? (w >> 16) : (w & 0xFFFF));
-        vb[q] = (short)((4 * grp + q < n) ? h : (uint16_t)0);
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q) o[t][q] *= al[q];
-      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, vb, o[t], 0, 0, 0);
-      o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa_lo, vb, o[t], 0, 0, 0);
-    }
+  for (int ch = ch0 + wave; ch < ch1; ch += 8) {
+    load_page(pb_, ch + 4);
+    process_page(pa_);
+    if (ch + 4 >= ch1) break;
+    load_page(pa_, ch + 8);
+    process_page(pb_);
   }
   // merge the 4 waves: lane `row` (grp 0) holds head row's (m, l); O rows are heads 4*grp + q
   if (grp == 0) { m_w[wave][row] = m_run; l_w[wave][row] = l_run; }
@@ -743,6 +785,8 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
       dst[dd] = num;
       if (dd == 0) { dst[HD] = mx; dst[HD + 1] = den; }
     }
+  }
+  __syncthreads();   // LDS is reused by the next item
   }
 }
 
@@ -798,8 +842,10 @@ __global__ __launch_bounds__(256) void k_sample_partial(const int32_t* __restric
     float* __restrict__ best, int32_t* __restrict__ bidx) {
   __shared__ float sb[256];
   __shared__ int si[256];
-  const int i = blockIdx.x, c = blockIdx.y;
-  if (i >= *M_ptr) return;
+  // persistent over (row, vocabulary chunk) items of the live rows
+  const int M = *M_ptr;
+  for (int item = blockIdx.x; item < M * kSampleChunks; item += gridDim.x) {
+  const int i = item / kSampleChunks, c = item - i * kSampleChunks;
   const int rid = rows ? rows[i].rid : rid_arr[i];
   const int gen = rows ? rows[i].gen : pos_arr[i];
   if (cpd) { seed = cpd->seed; step = cpd->step; temp = cpd->temperature; }
@@ -842,6 +888,8 @@ __global__ __launch_bounds__(256) void k_sample_partial(const int32_t* __restric
   if (threadIdx.x == 0) {
     best[(size_t)i * kSampleChunks + c] = sb[0];
     bidx[(size_t)i * kSampleChunks + c] = si[0];
+  }
+  __syncthreads();   // sb/si are reused by the next item
   }
 }
 
@@ -944,7 +992,8 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     const bool wide = N >= 65536;
     const int rows_per_block = wide ? 128 : 64;
     int tiles_n = (N + rows_per_block - 1) / rows_per_block;
-    int zb = (M_cap + 16 * MT - 1) / (16 * MT);
+    // decode: one z block loops over the live m-blocks; prefill: exact m-blocks
+    int zb = c->in_prefill ? (M_cap + 16 * MT - 1) / (16 * MT) : 1;
     int want = (tiles_n >= 256) ? 1 : (256 + tiles_n - 1) / tiles_n;
     // 64-wide k chunks: four pipeline slots of X + W fit in registers for NT <= 2
     const int KC = 64;
@@ -996,13 +1045,19 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
 static void gemm_swiglu(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr, int M_cap) {
   constexpr int MT = 8;
   const int N = 2 * c->ffn, K = c->d;
-  dim3 grid((N + 127) / 128, 1, (M_cap + 16 * MT - 1) / (16 * MT));
+  dim3 grid((N + 127) / 128, 1, c->in_prefill ? (M_cap + 16 * MT - 1) / (16 * MT) : 1);
   if (c->in_prefill)
     hipLaunchKernelGGL((k_gemm_bf16_lds<2, MT, 64, 1, 1>), grid, dim3(256), 0, c->stream, (const uint16_t*)X,
                        (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0);
   else
     hipLaunchKernelGGL((k_gemm_bf16_lds<2, MT, 64, 1, 0>), grid, dim3(256), 0, c->stream, (const uint16_t*)X,
                        (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0);
+}
+
+// persistent attention grid: enough blocks for two per CU, never more than items
+static int attn_grid(sara_ctx* c, int M_cap) {
+  int items = M_cap * c->hkv * c->attn_splits_max;
+  return std::max(1, std::min(items, 1024));
 }
 
 template <typename T, int HD>
@@ -1020,7 +1075,7 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     if (mfma_attn && !c->in_prefill) {
       // decode: q|k|v epilogue, attention and split merge in one kernel
       PROF_B(c);
-      hipLaunchKernelGGL((k_attn_mfma<HD, 1>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
+      hipLaunchKernelGGL((k_attn_mfma<HD, 1>), dim3(attn_grid(c, M_cap)), dim3(256), 0, st,
                          M_ptr, c->rows, (const uint16_t*)c->qbuf, (uint16_t*)c->kc, (uint16_t*)c->vc, c->btab,
                          c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv, c->attn_splits_max,
                          1.0f / sqrtf((float)HD), c->attn_part, (const float*)c->ws, sp, stride_qkv, c->rope,
@@ -1039,7 +1094,7 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     PROF_E(c, kPQkv, c->nqkv, 0);
     PROF_B(c);
     if (mfma_attn)
-      hipLaunchKernelGGL((k_attn_mfma<HD, 0>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
+      hipLaunchKernelGGL((k_attn_mfma<HD, 0>), dim3(attn_grid(c, M_cap)), dim3(256), 0, st,
                          M_ptr, c->rows, (const uint16_t*)c->qbuf, (uint16_t*)c->kc,
                          (uint16_t*)c->vc, c->btab, c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv,
                          c->attn_splits_max, 1.0f / sqrtf((float)HD), c->attn_part, (const float*)nullptr, 0,
@@ -1151,7 +1206,7 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
     gemm(c, c->x, c->lm_head, c->rows_M, S, c->V, c->d, sp, 1);
     PROF_E(c, kPGemmLM, c->V, c->d);
     PROF_B(c);
-    hipLaunchKernelGGL(k_sample_partial, dim3(S, kSampleChunks), dim3(256), 0, st, c->rows_M,
+    hipLaunchKernelGGL(k_sample_partial, dim3(std::min(S * kSampleChunks, 2048)), dim3(256), 0, st, c->rows_M,
                        (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, c->ws, c->V,
                        (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, c->samp_best, c->samp_idx);
     PROF_E(c, kPSampleP, c->V, 0);
@@ -1185,7 +1240,8 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
   if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
   e = hipMemcpyAsync(mdev, &n_rows, sizeof(int32_t), hipMemcpyHostToDevice, st);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
-  hipLaunchKernelGGL(k_sample_partial, dim3(n_rows, kSampleChunks), dim3(256), 0, st, mdev, rid, pos,
+  hipLaunchKernelGGL(k_sample_partial, dim3(std::min(n_rows * kSampleChunks, 2048)), dim3(256), 0, st, mdev,
+                     rid, pos,
                      (const RowDesc*)nullptr, logits, V, (const CtlParams*)nullptr, seed, step, temp,
                      best, bidx);
   hipLaunchKernelGGL(k_sample_rows_final, dim3((n_rows + 255) / 256), dim3(256), 0, st, n_rows, rid,

@@ -1,0 +1,98 @@
+"""Full-size parity on the Qwen2.5-1.5B-shaped workload in the launch
+configuration bench.py times (HIP-graph replay, 512 slots, 1024 new tokens).
+
+The oracle cannot generate a full step, so it checks what it can compute
+one by one or what holds at any size:
+* controller: the oracle's event simulation fed the GPU's per-rollout
+  (length, reward) reproduces every decision, draw, assignment and finish
+  bit-exactly (p_eff within 1e-12);
+* reward: the oracle's hash chain over each rollout's GPU tokens gives the
+  GPU's reward;
+* GRPO advantages of the committed groups;
+* tokens: at sampled positions of sampled rollouts, the oracle's own logits
+  (one teacher-forced forward over the GPU's tokens) and sampler give the
+  GPU's token (bf16 rounding noise flips a near tie now and then, so >= 90%
+  agreement is required);
+* invariants: budget, lengths, committed groups mixed, token count."""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import controller as OC
+from oracle import grpo as OG
+from oracle import reward as OR
+from oracle import sampler as OS
+from oracle.model import Decoder
+from tests.gpu_harness import compare_logs, device_setup, run_gpu_step
+
+pytestmark = pytest.mark.gpu
+
+
+def test_full_size_qwen1p5b_step():
+    import torch
+    assert torch.cuda.is_available()
+    cfg = W.get_config("qwen1p5b_shape")
+    a, m = cfg["alloc"], cfg["model"]
+    k, U = a["k"], a["pool_U"]
+    pool = W.make_pool(cfg, 0)
+    seed = W.sampling_seed(cfg)
+    ctx, w = device_setup(cfg)
+    print("[full] running the GPU step (graph replay)", flush=True)
+    gpu = run_gpu_step(ctx, cfg, pool, use_graph=True)
+    ctx.close()
+    st = gpu["stats"]
+    print(f"[full] GPU: {st['rollouts']} rollouts, {st['tokens']} tokens, {st['committed']} committed, "
+          f"{st['decode_steps']} decode steps", flush=True)
+    fin = gpu["logs"]["finishes"]
+    outcome = {(int(u), int(j)): (int(L), int(r)) for (t, s, u, j, L, r) in fin}
+
+    # controller replay
+    ora = OC.simulate(a, U, lambda pairs: [outcome[p] for p in pairs])
+    compare_logs(gpu["logs"], ora)
+    assert (st["committed"], st["rollouts"], st["tokens"], st["decode_steps"], st["budget_left"]) == (
+        ora["n_committed"], ora["rollouts"], ora["tokens"], ora["decode_steps"], ora["budget_left"])
+
+    # rewards from the GPU's tokens, lengths and invariants
+    ro = gpu["roll"]
+    for (u, j), (L, r) in outcome.items():
+        toks = ro["tokens"][u * k + j][:L]
+        assert L <= a["max_new"] and np.all(toks >= 0)
+        h = OR.hash_tokens(seed, pool["step"], u, toks)
+        assert OR.reward_of_hash(h, float(pool["p"][u])) == r == ro["reward"][u * k + j]
+    assert st["rollouts"] <= a["budget_N"] and st["tokens"] == sum(L for L, _ in outcome.values())
+    for u in ora["committed"]:
+        assert 1 <= ora["successes"][u] <= ora["n_done"][u] - 1
+
+    # GRPO advantages
+    off, rw, adv = gpu["adv"]
+    offs, rws = [0], []
+    for u in ora["committed"]:
+        rws += [outcome[(u, j)][1] for j in range(ora["n_issued"][u])]
+        offs.append(len(rws))
+    assert np.array_equal(off, np.array(offs))
+    assert np.allclose(adv, OG.advantages(rws, offs), rtol=1e-6, atol=1e-6)
+
+    # tokens at sampled positions, from the oracle's logits
+    dec = Decoder(m, w)
+    g = np.random.default_rng(0)
+    keys = sorted(outcome)
+    picks = [keys[i] for i in g.choice(len(keys), size=3, replace=False)]
+    agree, total = 0, 0
+    for (u, j) in picks:
+        L = outcome[(u, j)][0]
+        prompt = pool["tokens"][pool["offsets"][u]:pool["offsets"][u + 1]]
+        P = len(prompt)
+        gen = ro["tokens"][u * k + j][:L]
+        pos = sorted(set([0, L - 1] + list(g.choice(L, size=6, replace=False))))
+        seq = np.concatenate([prompt, gen[:max(pos)]])
+        cache = dec.new_cache(len(seq))
+        logits = dec.forward(seq, np.arange(len(seq)), cache, logit_rows=[P - 1 + i for i in pos])
+        for n, i in enumerate(pos):
+            tok, sc = OS.sample(logits[n], a["temperature"], seed, pool["step"], u * k + j, i)
+            if m["eos_id"] >= 0 and OS.forced_eos(seed, pool["step"], u * k + j, i, a["forced_eos_u32"]):
+                tok = m["eos_id"]
+            agree += int(tok == ro["sampled"][u * k + j][i])
+            total += 1
+        print(f"[full] rollout ({u},{j}) L={L}: checked positions {pos}", flush=True)
+    print(f"[full] sampled-position agreement {agree}/{total}", flush=True)
+    assert agree >= 0.9 * total
