@@ -145,49 +145,55 @@ __global__ __launch_bounds__(256) void k_embed_norm(const int32_t* __restrict__ 
 // ---------------------------------------------------------------------------
 // GEMM: out[s][m][n] = sum_{k in split s} X[m][k] * W[n][k]
 // ---------------------------------------------------------------------------
-// bf16 MFMA GEMM with the activation tile in LDS.  Block = 4 waves; wave w
-// owns weight rows [n0, n0 + 16*NT) and all 16*MT activation rows of the
-// block's m-range.  The k loop is a 4-slot software pipeline: stage s loads
-// the X chunk (block-cooperative) and the wave's W chunk for k chunk s into
-// register slot s % 4, three stages ahead of its use; at its turn the X
-// chunk is written to one of two LDS buffers, and the MFMAs read X from LDS
-// and W from registers.  Loads of one stage are issued together, so waiting
-// for the oldest stage leaves the three younger ones in flight.
+// bf16 weights are stored fragment-major ("tiled") by sara_init: for each
+// 16-row tile and each 32-wide k step, the 64 lanes' 16-byte MFMA A-operand
+// fragments lie back to back (lane l holds row l % 16, k 8*(l/16)..+8), so
+// every weight load of a wave is one contiguous, fully coalesced 1 KiB read
+// and a wave walks its 16 rows as one sequential stream.
+__device__ __forceinline__ int64_t tiled_index(int64_t row, int64_t k, int64_t K) {
+  const int64_t tile = row >> 4, ks = k >> 5, lane = (row & 15) + 16 * ((k >> 3) & 3);
+  return ((tile * (K >> 5) + ks) * 64 + lane) * 8 + (k & 7);
+}
+
+// One m-block of MT 16-row tiles.  Block = 4 waves; wave w owns weight rows
+// [n0, n0 + 16*NT) and all 16*MT activation rows.  The k loop is a 4-slot
+// software pipeline: stage s loads the X chunk (block-cooperative) and the
+// wave's W chunk for k chunk s into register slot s % 4, three stages ahead
+// of its use; at its turn the X chunk goes to one of two LDS buffers and the
+// MFMAs read X from LDS and W from registers.  The loop has no peeled
+// prologue (its first trip only loads), so the wait counts the compiler
+// derives at the loop header are exact and three stages stay in flight.
 //
 // EPI = 0: fp32 partial sums to out[split][m][n].
 // EPI = 1: SwiGLU epilogue (one split only): the weight rows are interleaved
 //          per 16-row tile as gate (even tiles) and up (odd tiles) of the same
 //          16 features; out receives bf16 silu(g) * u as [m][N/2].
-// PF only separates the prefill instances from the decode ones in profiles.
-template <int NT, int MT, int KC, int EPI, int PF>
-__global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __restrict__ X,
-    const uint16_t* __restrict__ W, void* __restrict__ out, const int32_t* __restrict__ M_ptr,
-    int N, int K, int kps, int64_t split_stride) {
+template <int NT, int MT, int KC, int EPI>
+__device__ __forceinline__ void gemm_mblock(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
+    void* __restrict__ out, int M, int m_base, int N, int K, int kps, int64_t split_stride,
+    uint16_t* __restrict__ xs) {
   constexpr int MR = 16 * MT;
   constexpr int PITCH = KC + 8;                 // halves: rows shift by 4 banks, conflict-free b128 reads
-  constexpr int XU = MR * (KC / 8) / 256;       // uint4 per thread per X chunk
-  constexpr int CPK = KC / 32;                  // 16x16x32 MFMA k steps per chunk
   constexpr int C8 = KC / 8;                    // uint4 per X row per chunk
-  constexpr int RING = 4;
-  __shared__ __attribute__((aligned(16))) uint16_t xs[2][MR * PITCH];
-  const int M = *M_ptr;
-  // m-blocks of 16*MT rows: one per grid z (prefill) or all of them in turn
-  // (decode launches with grid z = 1 since M lives on the device)
-  for (int m_base = blockIdx.z * MR; m_base < M; m_base += gridDim.z * MR) {
+  constexpr int XU = (MR * C8 + 255) / 256;     // uint4 per thread per X chunk
+  constexpr int CPK = KC / 32;                  // 16x16x32 MFMA k steps per chunk
+  constexpr int BUF = MR * PITCH;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = lane & 15, grp = lane >> 4;
   const int n0 = (blockIdx.x * 4 + wave) * 16 * NT;
   const int k_begin = blockIdx.y * kps;
   const int k_end = min(K, k_begin + kps);
   const int nchunks = (k_end - k_begin) / KC;
-  // element offsets (32-bit: rows * K < 2^31 for every supported shape)
+  // element offsets (32-bit: N * K < 2^31 for every supported shape)
   int woff[NT];
 #pragma unroll
-  for (int nt = 0; nt < NT; ++nt) woff[nt] = min(n0 + 16 * nt + row, N - 1) * K + 8 * grp + k_begin;
+  for (int nt = 0; nt < NT; ++nt)
+    woff[nt] = (min(n0 / 16 + nt, N / 16 - 1) * (K / 32) + k_begin / 32) * 512 + lane * 8;
   int xoff[XU], xdst[XU];
 #pragma unroll
   for (int q = 0; q < XU; ++q) {
-    int u = threadIdx.x + 256 * q;
+    // threads past the tile repeat its last element (same value, same place)
+    int u = min((int)threadIdx.x + 256 * q, MR * C8 - 1);
     int rr = u / C8, c8 = u % C8;
     xoff[q] = min(m_base + rr, M - 1) * K + 8 * c8 + k_begin;
     xdst[q] = rr * PITCH + 8 * c8;
@@ -202,20 +208,20 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __rest
 #pragma unroll
     for (int t = 0; t < MT; ++t) acc[nt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int last = max(nchunks - 1, 0);
-  // loads are unconditional (clamped to the last chunk); surplus loads are unused
+  // loads are unconditional (clamped into [0, last]); surplus loads are unused
   auto load = [&](Stage& st, int chunk) {
-    const int kk = min(chunk, last) * KC;
+    const int kk = max(min(chunk, last), 0) * KC;
 #pragma unroll
     for (int q = 0; q < XU; ++q) st.x[q] = *(const u32x4*)(X + xoff[q] + kk);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-      for (int cc = 0; cc < CPK; ++cc) st.w[nt][cc] = *(const u32x4*)(W + woff[nt] + kk + 32 * cc);
+      for (int cc = 0; cc < CPK; ++cc) st.w[nt][cc] = *(const u32x4*)(W + woff[nt] + kk * 16 + 512 * cc);
   };
   auto consume = [&](Stage& st, int buf, int ch) {
     // buffer `buf` was last read two chunks ago, before the previous barrier
 #pragma unroll
-    for (int q = 0; q < XU; ++q) *(u32x4*)&xs[buf][xdst[q]] = st.x[q];
+    for (int q = 0; q < XU; ++q) *(u32x4*)&xs[buf * BUF + xdst[q]] = st.x[q];
     __syncthreads();
     if (ch < nchunks) {
       // rows past M read a clamped (valid) X row; their results are never stored
@@ -223,7 +229,7 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __rest
       for (int t = 0; t < MT; ++t) {
 #pragma unroll
         for (int cc = 0; cc < CPK; ++cc) {
-          u32x4 xv = *(const u32x4*)&xs[buf][(16 * t + row) * PITCH + 8 * grp + 32 * cc];
+          u32x4 xv = *(const u32x4*)&xs[buf * BUF + (16 * t + row) * PITCH + 8 * grp + 32 * cc];
 #pragma unroll
           for (int nt = 0; nt < NT; ++nt)
             acc[nt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
@@ -232,18 +238,18 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __rest
       }
     }
   };
-  load(s0, 0);
-  load(s1, 1);
-  load(s2, 2);
-  for (int base = 0; base < nchunks; base += RING) {
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): nothing of an earlier m-block is still pending
+  int base0 = -4;
+  asm volatile("" : "+s"(base0));       // opaque start: the first (load-only) trip stays in the loop
+  for (int base = base0; base < nchunks; base += 4) {
     load(s3, base + 3);
-    consume(s0, 0, base);
+    if (base >= 0) consume(s0, 0, base);
     load(s0, base + 4);
-    consume(s1, 1, base + 1);
+    if (base >= 0) consume(s1, 1, base + 1);
     load(s1, base + 5);
-    consume(s2, 0, base + 2);
+    if (base >= 0) consume(s2, 0, base + 2);
     load(s2, base + 6);
-    consume(s3, 1, base + 3);
+    if (base >= 0) consume(s3, 1, base + 3);
   }
   if (EPI == 0) {
     float* o = (float*)out + (size_t)blockIdx.y * split_stride;
@@ -280,7 +286,44 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __rest
       }
     }
   }
-  __syncthreads();   // the LDS tiles are reused by the next m-block
+}
+
+// bf16 MFMA GEMM over tiled weights.  The live row count M is read on the
+// device; each m-block of up to 16*MTMAX rows runs the instance with just
+// enough 16-row tiles (ceil(rows / 16)), so small batches spend no MFMA,
+// LDS or X traffic on empty tiles.  Decode launches use grid z = 1 and loop
+// over the m-blocks; prefill launches one z block per m-block.
+// PF only separates the prefill instances from the decode ones in profiles.
+template <int NT, int MTMAX, int KC, int EPI, int PF>
+__global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __restrict__ X,
+    const uint16_t* __restrict__ W, void* __restrict__ out, const int32_t* __restrict__ M_ptr,
+    int N, int K, int kps, int64_t split_stride) {
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2 * 16 * MTMAX * (KC + 8)];
+  const int M = *M_ptr;
+  for (int m_base = blockIdx.z * 16 * MTMAX; m_base < M; m_base += gridDim.z * 16 * MTMAX) {
+    const int mt = min(MTMAX, (M - m_base + 15) >> 4);
+#define SARA_MB(c) \
+    if constexpr (MTMAX >= c) { \
+      if (mt == c) gemm_mblock<NT, c, KC, EPI>(X, W, out, M, m_base, N, K, kps, split_stride, xs); \
+    }
+    SARA_MB(1) SARA_MB(2) SARA_MB(3) SARA_MB(4) SARA_MB(5) SARA_MB(6) SARA_MB(7) SARA_MB(8)
+#undef SARA_MB
+    __syncthreads();   // the LDS tiles are reused by the next m-block
+  }
+}
+
+// Row-major [n_tiles*16][K] bf16 -> fragment-major tiles (see tiled_index);
+// source tile j lands in destination tile j * tile_mul + tile_add, which
+// builds the fused q|k|v and the gate/up-interleaved matrices in place.
+__global__ void k_tile_weights(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst, int n_tiles,
+                               int K, int tile_mul, int tile_add) {
+  const int64_t per_tile = (int64_t)16 * K;
+  const int64_t total = per_tile * n_tiles;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int64_t r = e / K, k = e - r * K;
+    const int64_t j = r >> 4;
+    const int64_t drow = (j * tile_mul + tile_add) * 16 + (r & 15);
+    dst[tiled_index(drow, k, K)] = src[e];
   }
 }
 
@@ -984,13 +1027,14 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
                 int N, int K, int& splits_out, int max_splits = 1 << 30) {
   int64_t stride = (int64_t)M_cap * N;
   if (c->md.dtype == SARA_BF16) {
-    // weight rows per block: 128 for very wide outputs (LM head), else 64;
-    // split K until the grid has about one block per CU (each split keeps
-    // >= 4 k chunks): wide GEMMs need no split, narrow ones trade fp32
-    // partial traffic for occupancy
+    // weight rows per block: 128 (two 16-row tiles per wave) for the LM head
+    // and long-K GEMMs, 64 otherwise; split K until the grid has about one
+    // block per CU (each split keeps >= 4 k chunks): wide GEMMs need no
+    // split, narrow ones trade fp32 partial traffic for occupancy
     constexpr int MT = 8;
     const bool wide = N >= 65536;
-    const int rows_per_block = wide ? 128 : 64;
+    const bool two = wide || K >= 4096;
+    const int rows_per_block = two ? 128 : 64;
     int tiles_n = (N + rows_per_block - 1) / rows_per_block;
     // decode: one z block loops over the live m-blocks; prefill: exact m-blocks
     int zb = c->in_prefill ? (M_cap + 16 * MT - 1) / (16 * MT) : 1;
@@ -1011,10 +1055,10 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     hipLaunchKernelGGL((k_gemm_bf16_lds<NT_, MT, KC_, 0, PF_>), grid, dim3(256), 0, c->stream, Xh, Wh, \
                        (void*)c->ws, M_ptr, N, K, kps, stride)
     if (c->in_prefill) {
-      if (wide) SARA_GEMM(2, 64, 1);
+      if (two) SARA_GEMM(2, 64, 1);
       else SARA_GEMM(1, 64, 1);
     } else {
-      if (wide) SARA_GEMM(2, 64, 0);
+      if (two) SARA_GEMM(2, 64, 0);
       else SARA_GEMM(1, 64, 0);
     }
 #undef SARA_GEMM
@@ -1254,22 +1298,11 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
   return SARA_OK;
 }
 
-// W_gu for the SwiGLU epilogue: 16-row tile 2j = gate rows [16j, 16j+16),
-// tile 2j+1 = up rows [16j, 16j+16)
-__global__ void k_interleave_gate_up(const uint16_t* __restrict__ wg, const uint16_t* __restrict__ wu,
-                                     uint16_t* __restrict__ dst, int ffn, int d) {
-  const size_t total = (size_t)2 * ffn * d;
-  for (size_t e = (size_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (size_t)gridDim.x * 256) {
-    size_t r = e / d, col = e - r * d;
-    size_t tile = r >> 4, within = r & 15;
-    size_t src_row = (tile >> 1) * 16 + within;
-    dst[e] = (tile & 1) ? wu[src_row * d + col] : wg[src_row * d + col];
-  }
-}
-
-int launch_interleave_gate_up(sara_ctx* c, const void* wg, const void* wu, void* dst) {
-  hipLaunchKernelGGL(k_interleave_gate_up, dim3(2048), dim3(256), 0, c->stream, (const uint16_t*)wg,
-                     (const uint16_t*)wu, (uint16_t*)dst, c->ffn, c->d);
+// Tiled copy of a row-major bf16 weight [rows][K] (rows a multiple of 16)
+// into dst, source tile j going to destination tile j * tile_mul + tile_add.
+int launch_tile_weights(sara_ctx* c, const void* src, void* dst, int rows, int K, int tile_mul, int tile_add) {
+  hipLaunchKernelGGL(k_tile_weights, dim3(2048), dim3(256), 0, c->stream, (const uint16_t*)src, (uint16_t*)dst,
+                     rows / 16, K, tile_mul, tile_add);
   return SARA_OK;
 }
 

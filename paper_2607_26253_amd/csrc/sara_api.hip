@@ -218,7 +218,7 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
     int r_ = dmalloc((void**)&(ptr), (size_t)(bytes), own); \
     if (r_) { sara_destroy(c); return r_; }                 \
   } while (0)
-  // weights, repacked: q|k|v rows fused, gate|up rows fused
+  // weights, repacked: q|k|v rows fused, gate|up rows fused (bf16: tiled, see launch_tile_weights)
   ALLOC(c->embed, (size_t)c->V * d * E);
   ALLOC(c->lm_head, (size_t)c->V * d * E);
   c->w_qkv.resize(c->L); c->w_o.resize(c->L); c->w_gu.resize(c->L); c->w_d.resize(c->L);
@@ -299,24 +299,38 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   const size_t qb = (size_t)c->qdim * d * E, kvb = (size_t)c->hkv * c->hd * d * E;
   const size_t fb = (size_t)c->ffn * d * E;
   hipError_t e = cp(c->embed, d_weights[0], (size_t)c->V * d * E);
-  for (int l = 0; l < c->L && e == hipSuccess; ++l) {
-    const void* const* w = d_weights + 1 + 9 * l;
-    char* qkv = (char*)c->w_qkv[l];
-    e = cp(qkv, w[1], qb);
-    if (e == hipSuccess) e = cp(qkv + qb, w[2], kvb);
-    if (e == hipSuccess) e = cp(qkv + qb + kvb, w[3], kvb);
-    if (e == hipSuccess) e = cp(c->w_o[l], w[4], (size_t)d * c->qdim * E);
-    char* gu = (char*)c->w_gu[l];
-    if (md->dtype == SARA_BF16) {
-      // tile-interleaved gate|up rows for the fused SwiGLU epilogue
-      if (e == hipSuccess) launch_interleave_gate_up(c, w[6], w[7], gu);
-    } else {
+  if (md->dtype == SARA_BF16) {
+    // GEMM weights in the fragment-major tiled layout of the bf16 GEMM
+    const int kvr = c->hkv * c->hd;
+    for (int l = 0; l < c->L && e == hipSuccess; ++l) {
+      const void* const* w = d_weights + 1 + 9 * l;
+      launch_tile_weights(c, w[1], c->w_qkv[l], c->qdim, d, 1, 0);
+      launch_tile_weights(c, w[2], c->w_qkv[l], kvr, d, 1, c->qdim / 16);
+      launch_tile_weights(c, w[3], c->w_qkv[l], kvr, d, 1, (c->qdim + kvr) / 16);
+      launch_tile_weights(c, w[4], c->w_o[l], d, c->qdim, 1, 0);
+      // gate and up tiles interleaved (gate tile j -> 2j, up tile j -> 2j + 1) for the SwiGLU epilogue
+      launch_tile_weights(c, w[6], c->w_gu[l], c->ffn, d, 2, 0);
+      launch_tile_weights(c, w[7], c->w_gu[l], c->ffn, d, 2, 1);
+      launch_tile_weights(c, w[8], c->w_d[l], d, c->ffn, 1, 0);
+      e = hipGetLastError();
+    }
+    launch_tile_weights(c, d_weights[2 + 9 * c->L], c->lm_head, c->V, d, 1, 0);
+    if (e == hipSuccess) e = hipGetLastError();
+  } else {
+    for (int l = 0; l < c->L && e == hipSuccess; ++l) {
+      const void* const* w = d_weights + 1 + 9 * l;
+      char* qkv = (char*)c->w_qkv[l];
+      e = cp(qkv, w[1], qb);
+      if (e == hipSuccess) e = cp(qkv + qb, w[2], kvb);
+      if (e == hipSuccess) e = cp(qkv + qb + kvb, w[3], kvb);
+      if (e == hipSuccess) e = cp(c->w_o[l], w[4], (size_t)d * c->qdim * E);
+      char* gu = (char*)c->w_gu[l];
       if (e == hipSuccess) e = cp(gu, w[6], fb);
       if (e == hipSuccess) e = cp(gu + fb, w[7], fb);
+      if (e == hipSuccess) e = cp(c->w_d[l], w[8], (size_t)d * c->ffn * E);
     }
-    if (e == hipSuccess) e = cp(c->w_d[l], w[8], (size_t)d * c->ffn * E);
+    if (e == hipSuccess) e = cp(c->lm_head, d_weights[2 + 9 * c->L], (size_t)c->V * d * E);
   }
-  if (e == hipSuccess) e = cp(c->lm_head, d_weights[2 + 9 * c->L], (size_t)c->V * d * E);
   if (e != hipSuccess) { sara_destroy(c); return hip_fail(e, "weight copy"); }
   rc = launch_convert_norms(c, d_weights);
   if (rc) { sara_destroy(c); return rc; }

@@ -187,7 +187,7 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
                        const int32_t* pos, uint64_t seed, int step, float temp, int eos,
                        uint32_t feos, int32_t* tok, hipStream_t st);
 int launch_convert_norms(sara_ctx* c, const void* const* w);
-int launch_interleave_gate_up(sara_ctx* c, const void* wg, const void* wu, void* dst);
+int launch_tile_weights(sara_ctx* c, const void* src, void* dst, int rows, int K, int tile_mul, int tile_add);
 
 // ---------------------------------------------------------------------------
 // device helpers
