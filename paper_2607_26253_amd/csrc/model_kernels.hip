@@ -377,6 +377,26 @@ __device__ __forceinline__ float split_sum(const float* ws, int splits, int64_t 
   return (a0 + a1) + (a2 + a3);
 }
 
+// Loads that only some threads or iterations need are written as
+// unconditional loads from a clamped, always valid address whose value is
+// then multiplied by a 0/1 mask (finite data, so x * 0 = 0 exactly).  A load
+// under a condition, or one whose value is only used under a condition,
+// becomes a branch that waits for the load before going on, which would
+// serialise the memory round trips.
+__device__ __forceinline__ float mask01(bool keep) { return keep ? 1.0f : 0.0f; }
+
+// split_sum for at most kMaxSplitsDec splits with every load in flight at once.
+__device__ __forceinline__ float split_sum8(const float* ws, int splits, int64_t stride, size_t idx) {
+  float v[kMaxSplitsDec];
+#pragma unroll
+  for (int s = 0; s < kMaxSplitsDec; ++s)
+    v[s] = ws[(size_t)min(s, splits - 1) * stride + idx] * mask01(s < splits);
+  float a[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < kMaxSplitsDec; ++s) a[s & 3] += v[s];
+  return (a[0] + a[1]) + (a[2] + a[3]);
+}
+
 // Page of position pos: block-table entries [0, PB) map the shared prompt
 // segment (positions < plen), entries [PB, MAXB) the private segment that
 // starts at position plen.
@@ -467,6 +487,69 @@ __global__ __launch_bounds__(1024) void k_residual_norm(const int32_t* __restric
     st_f32(x, idx, h[idx] * inv * w[c]);
   }
   __syncthreads();   // red[] is reused by the next row
+  }
+}
+
+// Same operation for rows of d <= 256 * VPT features and at most
+// kMaxSplitsDec splits: one 256-thread block per row, every thread owns VPT
+// features (c = threadIdx.x + 256 v) and keeps them in registers; the split
+// partials are summed in the order of split_sum with every load in flight at
+// once.
+template <typename T, int VPT>
+__global__ __launch_bounds__(256) void k_residual_norm_v(const int32_t* __restrict__ M_ptr,
+    const float* __restrict__ ws, int splits, int64_t stride, int d, float* __restrict__ h,
+    const float* __restrict__ w, float eps, T* __restrict__ x) {
+  __shared__ float red[4];
+  const int M = *M_ptr;
+  for (int i = blockIdx.x; i < M; i += gridDim.x) {
+    const size_t rb = (size_t)i * d;
+    float a0[VPT], a1[VPT], a2[VPT], a3[VPT], hv[VPT];
+    // unconditional loads from clamped indices, masked (see split_sum8)
+    float wv[VPT];
+#pragma unroll
+    for (int v = 0; v < VPT; ++v) {
+      const int c = min((int)threadIdx.x + 256 * v, d - 1);
+      a0[v] = a1[v] = a2[v] = a3[v] = 0.f;
+      hv[v] = h[rb + c] * mask01((int)threadIdx.x + 256 * v < d);
+      wv[v] = w[c];
+    }
+    float pv[kMaxSplitsDec][VPT];
+#pragma unroll
+    for (int s = 0; s < kMaxSplitsDec; ++s)
+#pragma unroll
+      for (int v = 0; v < VPT; ++v) {
+        const int c = min((int)threadIdx.x + 256 * v, d - 1);
+        pv[s][v] = ws[(size_t)min(s, splits - 1) * stride + rb + c] *
+                   mask01(s < splits && (int)threadIdx.x + 256 * v < d);
+      }
+#pragma unroll
+    for (int s = 0; s < kMaxSplitsDec; s += 4)
+#pragma unroll
+      for (int v = 0; v < VPT; ++v) {
+        a0[v] += pv[s][v];
+        a1[v] += pv[s + 1][v];
+        a2[v] += pv[s + 2][v];
+        a3[v] += pv[s + 3][v];
+      }
+    float ss = 0.f;
+#pragma unroll
+    for (int v = 0; v < VPT; ++v) {
+      const int c = threadIdx.x + 256 * v;
+      const float val = hv[v] + ((a0[v] + a1[v]) + (a2[v] + a3[v]));
+      hv[v] = val;
+      if (c < d) {
+        h[rb + c] = val;
+        ss += val * val;
+      }
+    }
+    const float tot = block_sum256(ss, red);
+    const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+#pragma unroll
+    for (int v = 0; v < VPT; ++v) {
+      const int c = threadIdx.x + 256 * v;
+      if (c < d) st_f32(x, rb + c, hv[v] * inv * wv[v]);
+    }
+    __syncthreads();   // red[] is reused by the next row
   }
 }
 
@@ -833,39 +916,322 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
   }
 }
 
+// Decode attention (bf16, MFMA), one block per (split c, row i, KV head g)
+// with splits of kDecPages pages.  Every wave owns kDecPpw consecutive pages
+// of the split and issues all of their K and V loads before anything else,
+// so a split costs one HBM round trip; the pages of a small batch spread over
+// several blocks per CU.  The page math is that of k_attn_mfma: S^T = K q^T
+// on v_mfma_f32_16x16x32_bf16, online softmax over the 4 lanes holding a
+// head's 16 scores, O += P V on v_mfma_f32_16x16x16bf16_1k with P as a bf16
+// hi + lo pair.
+//
+// The block also forms its query heads from the fused q|k|v GEMM partials
+// (split sum, rotate-half RoPE, bf16).  The split holding the row's newest
+// position computes that position's k and v, appends them to the row's
+// private KV page, and writes them into the registers of the wave whose page
+// holds the position (the page was loaded before the append).  A row with a
+// single split writes its normalised output straight to `out` ([row][hq][HD],
+// bf16); other rows leave per-split partials for k_attn_combine.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_dec(const int32_t* __restrict__ M_ptr,
+    const RowDesc* __restrict__ rows, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
+    const int32_t* __restrict__ btab, int MAXB, int PB, int layer, int64_t n_blocks, int hq,
+    int hkv, int n_splits, float scale, float* __restrict__ part,
+    const float* __restrict__ qkv_ws, int qkv_splits, int64_t qkv_stride,
+    const float2* __restrict__ rope, uint16_t* __restrict__ out) {
+  typedef short short4_ __attribute__((ext_vector_type(4)));
+  typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+  constexpr int DPL = HD / 4;     // dims per lane in the QK^T operands
+  constexpr int NCC = HD / 32;    // 16x16x32 MFMAs per page for QK^T
+  constexpr int NT = HD / 16;     // output tiles of 16 dims
+  constexpr int PPW = kDecPpw;
+  __shared__ float m_w[4][16], l_w[4][16];
+  __shared__ float o_w[4][16][HD + 1];
+  __shared__ __attribute__((aligned(16))) uint16_t q_s[kMaxGroup][HD];
+  __shared__ __attribute__((aligned(16))) uint16_t kn_s[HD];
+  __shared__ uint16_t vn_s[HD];
+  const int M = *M_ptr;
+  const int total = M * hkv * n_splits;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = lane & 15, grp = lane >> 4;
+  const int G = hq / hkv;
+  const int half = HD / 2;
+  for (int item = blockIdx.x; item < total; item += gridDim.x) {
+    const int c = item / (M * hkv);
+    const int i = (item - c * M * hkv) / hkv, g = item % hkv;
+    const RowDesc r = rows[i];
+    const int ctx = r.pos + 1;
+    const int pl = min(ctx, r.plen);                      // prompt positions attended
+    const int pc = (pl + 15) >> 4;                         // prompt pages
+    const int vcnt = ctx - pl;                             // private positions (>= 1)
+    const int nch = pc + ((vcnt + 15) >> 4);
+    const int ch0 = c * kDecPages;
+    if (ch0 >= nch) continue;
+    const int ch1 = min(nch, ch0 + kDecPages);
+    const bool has_new = (ch1 == nch);
+    const int32_t* bt = btab + (size_t)r.tab * MAXB;
+    int my_blk = 0;
+    if (lane < kDecPages && ch0 + lane < ch1) {
+      const int cl = ch0 + lane;
+      my_blk = bt[(cl < pc) ? cl : PB + (cl - pc)];
+    }
+    struct Pg { u32x4 k[NCC]; u32x2 v[NT]; int n; };
+    Pg pg[PPW];
+#pragma unroll
+    for (int p = 0; p < PPW; ++p) {
+      const int ch = ch0 + wave * PPW + p;
+      const int cv = (ch < ch1) ? ch : ch0;                // pages past the split re-read its first
+      int n;
+      if (cv < pc) n = min(16, pl - 16 * cv);
+      else n = min(16, vcnt - 16 * (cv - pc));
+      pg[p].n = (ch < ch1) ? n : 0;
+      const int blk = __shfl(my_blk, cv - ch0, 64);
+      const size_t pgi = ((size_t)layer * n_blocks + blk) * hkv + g;
+      const u32x4* kp = (const u32x4*)(kc + (pgi * kBlockTok + row) * HD + DPL * grp);
+#pragma unroll
+      for (int cc = 0; cc < NCC; ++cc) pg[p].k[cc] = kp[cc];
+      const uint16_t* vp = vc + pgi * (size_t)HD * kBlockTok + 4 * grp;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) pg[p].v[t] = *(const u32x2*)(vp + (size_t)(16 * t + row) * kBlockTok);
+    }
+    // query heads of this KV group, then the newest position's k and v:
+    // rotation pairs (dim cc, cc + HD/2); the G*HD/2 query pairs and (last
+    // split) the HD/2 key pairs and HD value dims are spread over the
+    // threads, kPairsPT per thread, all partial loads issued together
+    const size_t rb = (size_t)i * (size_t)((hq + 2 * hkv) * HD);
+    const int nq = G * half, nk = has_new ? half : 0, nv = has_new ? HD : 0;
+    {
+      constexpr int PT = (kMaxGroup * HD / 2 + HD / 2 + HD + 255) / 256;
+      float va[PT], vb[PT];
+      float2 cs[PT];
+#pragma unroll
+      for (int t = 0; t < PT; ++t) {
+        // column indices first (always valid), then unconditional loads
+        const int e = threadIdx.x + 256 * t;
+        int ca = 0, rp = 0;
+        if (e < nq) {
+          const int gh = e / half, cc = e - gh * half;
+          ca = (g * G + gh) * HD + cc;
+          rp = cc;
+        } else if (e < nq + nk) {
+          const int cc = e - nq;
+          ca = (hq + g) * HD + cc;
+          rp = cc;
+        } else if (e < nq + nk + nv) {
+          ca = (hq + hkv + g) * HD + (e - nq - nk);
+        }
+        const int cb = (e < nq + nk) ? ca + half : ca;
+        va[t] = split_sum8(qkv_ws, qkv_splits, qkv_stride, rb + ca);
+        vb[t] = split_sum8(qkv_ws, qkv_splits, qkv_stride, rb + cb);
+        cs[t] = rope[(size_t)r.pos * half + rp];
+      }
+#pragma unroll
+      for (int t = 0; t < PT; ++t) {
+        const int e = threadIdx.x + 256 * t;
+        const float a = va[t], b = vb[t];
+        const uint16_t r0 = f32_to_bf16(a * cs[t].x - b * cs[t].y), r1 = f32_to_bf16(b * cs[t].x + a * cs[t].y);
+        if (e < nq) {
+          const int gh = e / half, cc = e - gh * half;
+          q_s[gh][cc] = r0;
+          q_s[gh][cc + half] = r1;
+        } else if (e < nq + nk) {
+          const int cc = e - nq;
+          kn_s[cc] = r0;
+          kn_s[cc + half] = r1;
+          kc[kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc, r.pos)] = r0;
+          kc[kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc + half, r.pos)] = r1;
+        } else if (e < nq + nk + nv) {
+          const int cc = e - nq - nk;
+          const uint16_t v0 = f32_to_bf16(a);
+          vn_s[cc] = v0;
+          vc[vt_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc, r.pos)] = v0;
+        }
+      }
+    }
+    __syncthreads();
+    if (has_new) {
+      // the newest position is private token o_new of page nch - 1
+      const int rel = nch - 1 - ch0;
+      const int o_new = (vcnt - 1) & 15;
+      if (rel / PPW == wave) {
+#pragma unroll
+        for (int p = 0; p < PPW; ++p) {
+          if (p != rel % PPW) continue;
+          if (row == o_new) {
+#pragma unroll
+            for (int cc = 0; cc < NCC; ++cc) pg[p].k[cc] = *(const u32x4*)&kn_s[DPL * grp + 8 * cc];
+          }
+          if ((o_new >> 2) == grp) {
+            const int q = o_new & 3;
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+              const uint32_t nv = vn_s[16 * t + row];
+              uint32_t w = (q < 2) ? pg[p].v[t].x : pg[p].v[t].y;
+              w = (q & 1) ? ((w & 0x0000FFFFu) | (nv << 16)) : ((w & 0xFFFF0000u) | nv);
+              if (q < 2) pg[p].v[t].x = w; else pg[p].v[t].y = w;
+            }
+          }
+        }
+      }
+    }
+    // q operand: head `row` of this KV group (zero beyond G), dims [DPL*grp, DPL*grp + DPL)
+    uint4 qv[NCC];
+    if (row < G) {
+      const uint4* qp = (const uint4*)(&q_s[row][DPL * grp]);
+#pragma unroll
+      for (int cc = 0; cc < NCC; ++cc) qv[cc] = qp[cc];
+    } else {
+#pragma unroll
+      for (int cc = 0; cc < NCC; ++cc) qv[cc] = make_uint4(0, 0, 0, 0);
+    }
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x4 o[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int p = 0; p < PPW; ++p) {
+      const int n = pg[p].n;
+      if (n == 0) continue;
+      f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int cc = 0; cc < NCC; ++cc)
+        sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, pg[p].k[cc]),
+                                                     __builtin_bit_cast(bf16x8, qv[cc]), sc, 0, 0, 0);
+      // lane holds tokens 4*grp + q (q < 4) of head `row`
+      float sv[4];
+      float mt = -INFINITY;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        sv[q] = (4 * grp + q < n) ? sc[q] * scale : -INFINITY;
+        mt = fmaxf(mt, sv[q]);
+      }
+      mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
+      mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+      const float mn = fmaxf(m_run, mt);
+      const float alpha = expf(m_run - mn);
+      float ps = 0.f;
+      uint16_t pb[4], plo[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float pv = expf(sv[q] - mn);
+        const uint16_t bb = f32_to_bf16(pv);
+        pb[q] = bb;
+        plo[q] = f32_to_bf16(pv - bf16_to_f32(bb));
+        ps += pv;
+      }
+      ps += __shfl_xor(ps, 16, 64);
+      ps += __shfl_xor(ps, 32, 64);
+      l_run = l_run * alpha + ps;
+      m_run = mn;
+      float al[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) al[q] = __shfl(alpha, 4 * grp + q, 64);
+      short4_ pa, pa_lo;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { pa[q] = (short)pb[q]; pa_lo[q] = (short)plo[q]; }
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        // positions beyond the page's n valid tokens may hold stale bits: zero them
+        short4_ vb;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const uint32_t w = (q < 2) ? pg[p].v[t].x : pg[p].v[t].y;
+          const uint16_t h = (uint16_t)((q & 1) ? (w >> 16) : (w & 0xFFFF));
+          vb[q] = (short)((4 * grp + q < n) ? h : (uint16_t)0);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) o[t][q] *= al[q];
+        o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa, vb, o[t], 0, 0, 0);
+        o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(pa_lo, vb, o[t], 0, 0, 0);
+      }
+    }
+    // merge the 4 waves: lane `row` (grp 0) holds head row's (m, l); O rows are heads 4*grp + q
+    if (grp == 0) { m_w[wave][row] = m_run; l_w[wave][row] = l_run; }
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o_w[wave][4 * grp + q][16 * t + row] = o[t][q];
+    __syncthreads();
+    const int ns = (nch + kDecPages - 1) / kDecPages;
+    for (int e = threadIdx.x; e < G * HD; e += 256) {
+      const int h = e / HD, dd = e - h * HD;
+      const float mx = fmaxf(fmaxf(m_w[0][h], m_w[1][h]), fmaxf(m_w[2][h], m_w[3][h]));
+      float num = 0.f, den = 0.f;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const float wt = (m_w[w][h] == -INFINITY) ? 0.f : expf(m_w[w][h] - mx);
+        num += wt * o_w[w][h][dd];
+        den += wt * l_w[w][h];
+      }
+      if (ns == 1) {
+        out[((size_t)i * hq + g * G + h) * HD + dd] = f32_to_bf16(num / den);
+      } else {
+        float* dst = part + ((((size_t)i * hkv + g) * n_splits + c) * kMaxGroup + h) * (HD + 2);
+        dst[dd] = num;
+        if (dd == 0) { dst[HD] = mx; dst[HD + 1] = den; }
+      }
+    }
+    __syncthreads();   // LDS is reused by the next item
+  }
+}
+
 // merge the context splits of every (row, query head) into o (model dtype)
 // skip_single: rows with one split were written by the attention kernel.
+// One pass over the splits, eight at a time with all their loads in flight,
+// rescaling the running (max, numerator, denominator) as it goes.
 template <typename T, int HD>
 __global__ __launch_bounds__(HD) void k_attn_combine(const int32_t* __restrict__ M_ptr,
     const RowDesc* __restrict__ rows, const float* __restrict__ part, int hq, int hkv,
     int n_splits, int paged_splits, int skip_single, T* __restrict__ out) {
+  // paged_splits: pages per context split of the paged (bf16) attention
+  // kernels, 0 for the fp32 attention's token splits
   const int M = *M_ptr;
   for (int item = blockIdx.x; item < M * hq; item += gridDim.x) {
-  const int i = item / hq, h = item - i * hq;
-  int G = hq / hkv, g = h / G, gh = h - g * G;
-  const RowDesc r = rows[i];
-  int ctx = r.pos + 1;
-  int ns;
-  if (paged_splits) {
-    int pl = min(ctx, r.plen);
-    int nch = ((pl + 15) >> 4) + ((ctx - pl + 15) >> 4);
-    ns = (nch + kAttnChunks - 1) / kAttnChunks;
-  } else {
-    ns = (ctx + kAttnSplit - 1) / kAttnSplit;
-  }
-  if (skip_single && ns == 1) continue;
-  const float* base = part + (((size_t)i * hkv + g) * n_splits * kMaxGroup + gh) * (HD + 2);
-  const size_t sstride = (size_t)kMaxGroup * (HD + 2);
-  float mx = -INFINITY;
-  for (int c = 0; c < ns; ++c) mx = fmaxf(mx, base[c * sstride + HD]);
-  float num = 0.f, den = 0.f;
-  for (int c = 0; c < ns; ++c) {
-    const float* p = base + c * sstride;
-    float wgt = expf(p[HD] - mx);
-    num += wgt * p[threadIdx.x];
-    den += wgt * p[HD + 1];
-  }
-  st_f32(out, ((size_t)i * hq + h) * HD + threadIdx.x, num / den);
+    const int i = item / hq, h = item - i * hq;
+    const int G = hq / hkv, g = h / G, gh = h - g * G;
+    const RowDesc r = rows[i];
+    const int ctx = r.pos + 1;
+    int ns;
+    if (paged_splits) {
+      const int pl = min(ctx, r.plen);
+      const int nch = ((pl + 15) >> 4) + ((ctx - pl + 15) >> 4);
+      ns = (nch + paged_splits - 1) / paged_splits;
+    } else {
+      ns = (ctx + kAttnSplit - 1) / kAttnSplit;
+    }
+    if (skip_single && ns == 1) continue;
+    const float* base = part + (((size_t)i * hkv + g) * n_splits * kMaxGroup + gh) * (HD + 2);
+    const size_t sstride = (size_t)kMaxGroup * (HD + 2);
+    float mx = -INFINITY, num = 0.f, den = 0.f;
+    for (int c0 = 0; c0 < ns; c0 += 8) {
+      float pm[8], pl_[8], po[8];
+      float mk[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        // unconditional loads from a clamped split index (see split_sum8): the
+        // surplus entries repeat split ns - 1 of this chunk, which leaves the
+        // maximum unchanged, and their weight is masked to zero
+        const float* p = base + (size_t)min(c0 + q, ns - 1) * sstride;
+        pm[q] = p[HD];
+        pl_[q] = p[HD + 1];
+        po[q] = p[threadIdx.x];
+        mk[q] = mask01(c0 + q < ns);
+      }
+      float m2 = mx;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) m2 = fmaxf(m2, pm[q]);
+      const float sc = (mx == -INFINITY) ? 0.f : expf(mx - m2);
+      num *= sc;
+      den *= sc;
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float wgt = ((pm[q] == -INFINITY) ? 0.f : expf(pm[q] - m2)) * mk[q];
+        num += wgt * po[q];
+        den += wgt * pl_[q];
+      }
+      mx = m2;
+    }
+    st_f32(out, ((size_t)i * hq + h) * HD + threadIdx.x, num / den);
   }
 }
 
@@ -1033,7 +1399,7 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     // split, narrow ones trade fp32 partial traffic for occupancy
     constexpr int MT = 8;
     const bool wide = N >= 65536;
-    const bool two = wide || K >= 4096;
+    const bool two = wide || (K >= 4096 && c->in_prefill);
     const int rows_per_block = two ? 128 : 64;
     int tiles_n = (N + rows_per_block - 1) / rows_per_block;
     // decode: one z block loops over the live m-blocks; prefill: exact m-blocks
@@ -1043,6 +1409,8 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     const int KC = 64;
     int chunks = K / KC;
     int splits = std::min(want, std::max(1, chunks / 4));
+    // decode consumers sum at most kMaxSplitsDec partials in one batch of loads
+    if (!c->in_prefill) splits = std::min(splits, kMaxSplitsDec);
     if (splits > max_splits) splits = max_splits;
     if (splits < 1) splits = 1;
     int kps = ((chunks + splits - 1) / splits) * KC;
@@ -1104,6 +1472,29 @@ static int attn_grid(sara_ctx* c, int M_cap) {
   return std::max(1, std::min(items, 1024));
 }
 
+// h += split-K sum of ws; x = RMSNorm(h) * w
+template <typename T>
+static void residual_norm(sara_ctx* c, const int32_t* M_ptr, int M_cap, int sp, const float* w) {
+  const int d = c->d, vpt = (d + 255) / 256;
+  const dim3 grid(std::min(M_cap, 1024));
+  const int64_t stride = (int64_t)M_cap * d;
+  T* x = (T*)c->x;
+#define SARA_RN(V) hipLaunchKernelGGL((k_residual_norm_v<T, V>), grid, dim3(256), 0, c->stream, M_ptr, c->ws, \
+                                      sp, stride, d, c->h, w, c->md.rms_eps, x)
+  switch (sp <= kMaxSplitsDec ? vpt : 0) {
+    case 1: SARA_RN(1); break;
+    case 2: SARA_RN(2); break;
+    case 3: SARA_RN(3); break;
+    case 4: SARA_RN(4); break;
+    case 5: case 6: SARA_RN(6); break;
+    case 7: case 8: SARA_RN(8); break;
+    default:
+      hipLaunchKernelGGL(k_residual_norm<T>, dim3(std::min(M_cap, 256)), dim3(1024), 0, c->stream, M_ptr,
+                         c->ws, sp, stride, d, c->h, w, c->md.rms_eps, x);
+  }
+#undef SARA_RN
+}
+
 template <typename T, int HD>
 static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_norm_out) {
   hipStream_t st = c->stream;
@@ -1117,17 +1508,18 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     PROF_E(c, kPGemmN1, c->nqkv, d);
     const bool mfma_attn = (c->md.dtype == SARA_BF16);
     if (mfma_attn && !c->in_prefill) {
-      // decode: q|k|v epilogue, attention and split merge in one kernel
+      // decode: q|k|v epilogue and attention in one kernel, then the split merge
       PROF_B(c);
-      hipLaunchKernelGGL((k_attn_mfma<HD, 1>), dim3(attn_grid(c, M_cap)), dim3(256), 0, st,
-                         M_ptr, c->rows, (const uint16_t*)c->qbuf, (uint16_t*)c->kc, (uint16_t*)c->vc, c->btab,
-                         c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv, c->attn_splits_max,
+      const int dg = (int)std::min<int64_t>((int64_t)M_cap * c->hkv * c->dec_splits_max, 2048);
+      hipLaunchKernelGGL((k_attn_dec<HD>), dim3(dg), dim3(256), 0, st,
+                         M_ptr, c->rows, (uint16_t*)c->kc, (uint16_t*)c->vc, c->btab,
+                         c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv, c->dec_splits_max,
                          1.0f / sqrtf((float)HD), c->attn_part, (const float*)c->ws, sp, stride_qkv, c->rope,
                          (uint16_t*)x);
       PROF_E(c, kPAttn, 0, 0);
       PROF_B(c);
       hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(1024), dim3(HD), 0, st, M_ptr, c->rows,
-                         c->attn_part, c->hq, c->hkv, c->attn_splits_max, 1, 1, x);
+                         c->attn_part, c->hq, c->hkv, c->dec_splits_max, kDecPages, 1, x);
       PROF_E(c, kPCombine, 0, 0);
     } else {
     PROF_B(c);
@@ -1151,16 +1543,14 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     PROF_E(c, kPAttn, 0, 0);
     PROF_B(c);
     hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(1024), dim3(HD), 0, st, M_ptr, c->rows,
-                       c->attn_part, c->hq, c->hkv, c->attn_splits_max, mfma_attn ? 1 : 0, 0, x);
+                       c->attn_part, c->hq, c->hkv, c->attn_splits_max, mfma_attn ? kAttnChunks : 0, 0, x);
     PROF_E(c, kPCombine, 0, 0);
     }
     PROF_B(c);
     gemm(c, x, c->w_o[l], M_ptr, M_cap, d, c->qdim, sp);
     PROF_E(c, kPGemmN1, d, c->qdim);
     PROF_B(c);
-    hipLaunchKernelGGL(k_residual_norm<T>, dim3(std::min(M_cap, 256)), dim3(1024), 0, st, M_ptr, c->ws, sp,
-                       (int64_t)M_cap * d, d, c->h, c->norms + (size_t)(2 * l + 1) * d,
-                       c->md.rms_eps, x);
+    residual_norm<T>(c, M_ptr, M_cap, sp, c->norms + (size_t)(2 * l + 1) * d);
     PROF_E(c, kPResNorm, d, 0);
     if (c->md.dtype == SARA_BF16) {
       PROF_B(c);
@@ -1186,8 +1576,7 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     // the last layer's norm output is only needed when logits follow
     if (l + 1 < c->L || final_norm_out) {
       PROF_B(c);
-      hipLaunchKernelGGL(k_residual_norm<T>, dim3(std::min(M_cap, 256)), dim3(1024), 0, st, M_ptr, c->ws,
-                         sp, (int64_t)M_cap * d, d, c->h, nw, c->md.rms_eps, x);
+      residual_norm<T>(c, M_ptr, M_cap, sp, nw);
       PROF_E(c, kPResNorm, d, 0);
     }
   }

@@ -206,6 +206,7 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   c->row_cap = std::max(c->S, c->prefill_rows);
   c->attn_splits_max = std::max((c->max_pos + kAttnSplit - 1) / kAttnSplit,
                                 (c->MAXB + kAttnChunks - 1) / kAttnChunks);
+  c->dec_splits_max = (c->MAXB + kDecPages - 1) / kDecPages;
   {
     int64_t nd = std::max<int64_t>({c->V, c->nqkv, 2 * (int64_t)c->ffn, c->d});
     int64_t np = std::max<int64_t>({c->nqkv, 2 * (int64_t)c->ffn, c->d});
@@ -276,8 +277,10 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   ALLOC(c->qbuf, (size_t)c->row_cap * c->qdim * E);
   ALLOC(c->xa, (size_t)c->row_cap * c->ffn * E);
   ALLOC(c->ws, sizeof(float) * (size_t)c->ws_floats);
-  ALLOC(c->attn_part, sizeof(float) * (size_t)c->row_cap * c->hkv * c->attn_splits_max * kMaxGroup *
-                          (c->hd + 2));
+  ALLOC(c->attn_part, sizeof(float) *
+                          (size_t)std::max((int64_t)c->row_cap * c->attn_splits_max,
+                                           (int64_t)c->S * c->dec_splits_max) *
+                          c->hkv * kMaxGroup * (c->hd + 2));
   ALLOC(c->samp_best, sizeof(float) * (size_t)c->S * kSampleChunks);
   ALLOC(c->samp_idx, sizeof(int32_t) * (size_t)c->S * kSampleChunks);
   ALLOC(c->g_off, sizeof(int32_t) * (c->U + 1));

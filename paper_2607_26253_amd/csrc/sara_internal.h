@@ -16,7 +16,10 @@ namespace sara {
 // ---------------------------------------------------------------------------
 constexpr int kBlockTok = 16;        // KV page size in tokens
 constexpr int kAttnSplit = 256;      // tokens per context split (fp32 VALU attention)
-constexpr int kAttnChunks = 16;      // KV pages per context split (bf16 MFMA attention)
+constexpr int kAttnChunks = 16;      // KV pages per context split (bf16 MFMA prefill attention)
+constexpr int kDecPpw = 2;           // KV pages per wave in the decode attention
+constexpr int kDecPages = 4 * kDecPpw;  // KV pages per context split in the decode attention
+constexpr int kMaxSplitsDec = 8;     // split-K partials of a decode GEMM (summed in one batch)
 constexpr int kAttnTile = 64;        // tokens per LDS tile inside a split
 constexpr int kSampleChunks = 16;    // vocabulary chunks per sampled row
 constexpr int kCtlThreads = 1024;    // threads of the single-workgroup controller
@@ -77,6 +80,7 @@ struct sara_ctx {
   int elt = 2;                    // bytes per stored element (2 bf16, 4 fp32)
   int prefill_rows = 0;           // rows per prefill chunk
   int attn_splits_max = 0;
+  int dec_splits_max = 0;         // context splits of the decode attention
   int64_t ws_floats = 0;
 
   // weights (model dtype)
