@@ -49,6 +49,18 @@ __device__ float block_sum256(float v, float* red) {
   return r;
 }
 
+// Fragment-major ("tiled") layout of a [rows][K] bf16 matrix: for each
+// 16-row tile and each 32-wide k step, the 64 lanes' 16-byte MFMA operand
+// fragments lie back to back (lane l holds row l % 16, k 8*(l/16)..+8), so
+// every fragment load of a wave is one contiguous, fully coalesced 1 KiB read
+// and a wave walks its 16 rows as one sequential stream.  sara_init stores
+// the bf16 GEMM weights this way; the decode rows feeding the q|k|v kernel
+// are written this way too.
+__device__ __forceinline__ int64_t tiled_index(int64_t row, int64_t k, int64_t K) {
+  const int64_t tile = row >> 4, ks = k >> 5, lane = (row & 15) + 16 * ((k >> 3) & 3);
+  return ((tile * (K >> 5) + ks) * 64 + lane) * 8 + (k & 7);
+}
+
 // ---------------------------------------------------------------------------
 // embedding gather + first RMSNorm (decode and prefill rows)
 // ---------------------------------------------------------------------------
@@ -61,7 +73,9 @@ __global__ __launch_bounds__(256) void k_decode_embed(const Ctl* __restrict__ ct
     const int32_t* __restrict__ tok, const int32_t* __restrict__ off,
     const int32_t* __restrict__ out_tok, int k, int max_new, RowDesc* __restrict__ rows,
     int32_t* __restrict__ rows_M, int do_embed, const T* __restrict__ embed,
-    const float* __restrict__ w, int d, float eps, float* __restrict__ h, T* __restrict__ x) {
+    const float* __restrict__ w, int d, float eps, float* __restrict__ h, T* __restrict__ x,
+    int U, int PB, int SB, const float2* __restrict__ rope, int half, float2* __restrict__ row_rope,
+    int x_tiled) {
   __shared__ float red[4];
   const int M = ctl->done ? 0 : ctl->M;
   if (blockIdx.x == 0 && threadIdx.x == 0) *rows_M = M;
@@ -79,7 +93,11 @@ __global__ __launch_bounds__(256) void k_decode_embed(const Ctl* __restrict__ ct
     r.rid = rid;
     r.gen = g;
     r.uid = u;
+    r.kv0 = u * PB;
+    r.kv1 = U * PB + s * SB;
     if (threadIdx.x == 0) rows[i] = r;
+    // rotation angles of this row's position, read by every layer's q|k|v kernel
+    for (int e = threadIdx.x; e < half; e += 256) row_rope[(size_t)i * half + e] = rope[(size_t)r.pos * half + e];
     if (!do_embed) continue;
     float ss = 0.f;
     for (int cc = threadIdx.x; cc < d; cc += 256) {
@@ -90,7 +108,7 @@ __global__ __launch_bounds__(256) void k_decode_embed(const Ctl* __restrict__ ct
     float tot = block_sum256(ss, red);
     float inv = 1.0f / sqrtf(tot / (float)d + eps);
     for (int cc = threadIdx.x; cc < d; cc += 256)
-      st_f32(x, (size_t)i * d + cc, h[(size_t)i * d + cc] * inv * w[cc]);
+      st_f32(x, x_tiled ? (size_t)tiled_index(i, cc, d) : (size_t)i * d + cc, h[(size_t)i * d + cc] * inv * w[cc]);
     __syncthreads();   // red[] is reused by the next row
   }
 }
@@ -99,7 +117,7 @@ __global__ __launch_bounds__(256) void k_decode_embed(const Ctl* __restrict__ ct
 // prompt u (pre[u] <= r < pre[u+1]) and token t = r - pre[u].
 __global__ __launch_bounds__(256) void k_prefill_rows(const int32_t* __restrict__ pre, int U,
     int r0, int n, const int32_t* __restrict__ tok, const int32_t* __restrict__ off, int S,
-    RowDesc* __restrict__ rows, int32_t* __restrict__ rows_M) {
+    RowDesc* __restrict__ rows, int32_t* __restrict__ rows_M, int PB) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i == 0) *rows_M = n;
   if (i >= n) return;
@@ -119,6 +137,8 @@ __global__ __launch_bounds__(256) void k_prefill_rows(const int32_t* __restrict_
   d.rid = -1;
   d.gen = -1;
   d.uid = u;
+  d.kv0 = u * PB;
+  d.kv1 = -1;
   rows[i] = d;
 }
 
@@ -145,16 +165,6 @@ __global__ __launch_bounds__(256) void k_embed_norm(const int32_t* __restrict__ 
 // ---------------------------------------------------------------------------
 // GEMM: out[s][m][n] = sum_{k in split s} X[m][k] * W[n][k]
 // ---------------------------------------------------------------------------
-// bf16 weights are stored fragment-major ("tiled") by sara_init: for each
-// 16-row tile and each 32-wide k step, the 64 lanes' 16-byte MFMA A-operand
-// fragments lie back to back (lane l holds row l % 16, k 8*(l/16)..+8), so
-// every weight load of a wave is one contiguous, fully coalesced 1 KiB read
-// and a wave walks its 16 rows as one sequential stream.
-__device__ __forceinline__ int64_t tiled_index(int64_t row, int64_t k, int64_t K) {
-  const int64_t tile = row >> 4, ks = k >> 5, lane = (row & 15) + 16 * ((k >> 3) & 3);
-  return ((tile * (K >> 5) + ks) * 64 + lane) * 8 + (k & 7);
-}
-
 // One m-block of MT 16-row tiles.  Block = 4 waves; wave w owns weight rows
 // [n0, n0 + 16*NT) and all 16*MT activation rows.  The k loop is a 4-slot
 // software pipeline: stage s loads the X chunk (block-cooperative) and the
@@ -327,6 +337,29 @@ __global__ void k_tile_weights(const uint16_t* __restrict__ src, uint16_t* __res
   }
 }
 
+// Rotation-pair order of the bf16 q|k|v weight rows: within each head, the
+// 16-row tile j holds natural dims 8j..8j+7 (tile rows 0-7) and
+// HD/2 + 8j..HD/2 + 8j + 7 (tile rows 8-15), so both members of every
+// rotate-half pair (d, d + HD/2) land in one tile and in MFMA output lanes
+// l and l ^ 32.  Returns the stored row (output column) of dim d of head h.
+__host__ __device__ __forceinline__ int qkv_pair_col(int h, int d, int HD) {
+  const int half = HD / 2;
+  const int e = d < half ? d : d - half;
+  return h * HD + 16 * (e >> 3) + (e & 7) + (d < half ? 0 : 8);
+}
+
+// Row-major [n_rows][K] bf16 rows of heads head_off, head_off + 1, .. (HD
+// rows each, natural dim order) -> fragment-major tiles in rotation-pair order.
+__global__ void k_tile_weights_pairs(const uint16_t* __restrict__ src, uint16_t* __restrict__ dst, int n_rows,
+                                     int K, int head_off, int HD) {
+  const int64_t total = (int64_t)n_rows * K;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total; e += (int64_t)gridDim.x * 256) {
+    const int64_t r = e / K, k = e - r * K;
+    const int drow = qkv_pair_col(head_off + (int)(r / HD), (int)(r % HD), HD);
+    dst[tiled_index(drow, k, K)] = src[e];
+  }
+}
+
 // fp32 VALU GEMM for the fp32 model: 16x16 output tile per 256-thread block.
 __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ X,
     const float* __restrict__ W, float* __restrict__ out, const int32_t* __restrict__ M_ptr,
@@ -423,21 +456,23 @@ __device__ __forceinline__ size_t vt_index(const RowDesc& r, const int32_t* btab
 }
 
 // Split-K sum of the fused q|k|v output, rotate-half RoPE on q and k,
-// q -> bf16 buffer, k and v -> the row's KV page.
+// q -> bf16 buffer, k and v -> the row's KV page.  pair = 1: the GEMM output
+// columns are in rotation-pair order (bf16 weights, see qkv_pair_col).
 template <typename T>
 __global__ __launch_bounds__(256) void k_qkv_epilogue(const int32_t* __restrict__ M_ptr,
     const RowDesc* __restrict__ rows, const float* __restrict__ ws, int splits, int64_t stride,
     const float2* __restrict__ rope, int hq, int hkv, int hd, int layer, int64_t n_blocks,
     const int32_t* __restrict__ btab, int MAXB, int PB, T* __restrict__ qbuf, T* __restrict__ kc,
-    T* __restrict__ vc) {
+    T* __restrict__ vc, int pair) {
   const int half = hd >> 1, nh = hq + 2 * hkv, N = nh * hd;
   const int M = *M_ptr;
   for (int item = blockIdx.x; item < M * nh; item += gridDim.x) {
     const int i = item / nh, h = item - i * nh, c = threadIdx.x;
     const RowDesc r = rows[i];
-    size_t base = (size_t)i * N + (size_t)h * hd;
-    float a = split_sum(ws, splits, stride, base + c);
-    float b = split_sum(ws, splits, stride, base + c + half);
+    const int ca = pair ? qkv_pair_col(h, c, hd) : h * hd + c;
+    const int cb = pair ? qkv_pair_col(h, c + half, hd) : h * hd + c + half;
+    float a = split_sum(ws, splits, stride, (size_t)i * N + ca);
+    float b = split_sum(ws, splits, stride, (size_t)i * N + cb);
     if (h < hq + hkv) {
       float2 cs = rope[(size_t)r.pos * half + c];
       float ra = a * cs.x - b * cs.y;
@@ -464,7 +499,7 @@ __global__ __launch_bounds__(256) void k_qkv_epilogue(const int32_t* __restrict_
 template <typename T>
 __global__ __launch_bounds__(1024) void k_residual_norm(const int32_t* __restrict__ M_ptr,
     const float* __restrict__ ws, int splits, int64_t stride, int d, float* __restrict__ h,
-    const float* __restrict__ w, float eps, T* __restrict__ x) {
+    const float* __restrict__ w, float eps, T* __restrict__ x, int x_tiled) {
   __shared__ float red[16];
   const int M = *M_ptr;
   for (int i = blockIdx.x; i < M; i += gridDim.x) {
@@ -484,7 +519,7 @@ __global__ __launch_bounds__(1024) void k_residual_norm(const int32_t* __restric
   float inv = 1.0f / sqrtf(tot / (float)d + eps);
   for (int c = threadIdx.x; c < d; c += 1024) {
     size_t idx = (size_t)i * d + c;
-    st_f32(x, idx, h[idx] * inv * w[c]);
+    st_f32(x, x_tiled ? (size_t)tiled_index(i, c, d) : idx, h[idx] * inv * w[c]);
   }
   __syncthreads();   // red[] is reused by the next row
   }
@@ -498,7 +533,7 @@ __global__ __launch_bounds__(1024) void k_residual_norm(const int32_t* __restric
 template <typename T, int VPT>
 __global__ __launch_bounds__(256) void k_residual_norm_v(const int32_t* __restrict__ M_ptr,
     const float* __restrict__ ws, int splits, int64_t stride, int d, float* __restrict__ h,
-    const float* __restrict__ w, float eps, T* __restrict__ x) {
+    const float* __restrict__ w, float eps, T* __restrict__ x, int x_tiled) {
   __shared__ float red[4];
   const int M = *M_ptr;
   for (int i = blockIdx.x; i < M; i += gridDim.x) {
@@ -547,7 +582,7 @@ __global__ __launch_bounds__(256) void k_residual_norm_v(const int32_t* __restri
 #pragma unroll
     for (int v = 0; v < VPT; ++v) {
       const int c = threadIdx.x + 256 * v;
-      if (c < d) st_f32(x, rb + c, hv[v] * inv * wv[v]);
+      if (c < d) st_f32(x, x_tiled ? (size_t)tiled_index(i, c, d) : rb + c, hv[v] * inv * wv[v]);
     }
     __syncthreads();   // red[] is reused by the next row
   }
@@ -698,29 +733,18 @@ __global__ __launch_bounds__(256) void k_attention(const int32_t* __restrict__ M
 //                 split into bf16 hi + lo parts, two MFMAs)
 // The 4 waves' (max, sum, O) are merged in LDS into one partial per split.
 //
-// FUSE = 1 (decode rows): the block also forms its q heads from the fused
-// q|k|v GEMM partials (split sum, RoPE, bf16) and, if its split holds the
-// row's newest position, appends that position's k and v to the KV page
-// before reading it.  A row whose context fits one split writes its
-// normalised output straight to `out` ([row][hq][HD], bf16); other rows are
-// merged by the combine kernel.  (Merging in-kernel by the last-arriving
-// block would need a device-scope fence per block, which on this multi-XCD
-// part writes back the L2 and costs far more than a launch.)
-template <int HD, int FUSE>
+template <int HD>
 __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M_ptr,
     const RowDesc* __restrict__ rows, const uint16_t* __restrict__ qbuf,
-    uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
+    const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     const int32_t* __restrict__ btab, int MAXB, int PB, int layer, int64_t n_blocks, int hq,
-    int hkv, int n_splits, float scale, float* __restrict__ part,
-    const float* __restrict__ qkv_ws, int qkv_splits, int64_t qkv_stride,
-    const float2* __restrict__ rope, uint16_t* __restrict__ out) {
+    int hkv, int n_splits, float scale, float* __restrict__ part) {
   typedef short short4_ __attribute__((ext_vector_type(4)));
   constexpr int DPL = HD / 4;     // dims per lane in the QK^T operands
   constexpr int NCC = HD / 32;    // 16x16x32 MFMAs per page for QK^T
   constexpr int NT = HD / 16;     // output tiles of 16 dims
   __shared__ float m_w[4][16], l_w[4][16];
   __shared__ float o_w[4][16][HD + 1];
-  __shared__ __attribute__((aligned(16))) uint16_t q_s[kMaxGroup][HD];
   // persistent over work items (split c, row i, KV head g), split-major, so
   // that no block waits only to find its row absent
   const int M = *M_ptr;
@@ -835,44 +859,9 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
   };
   Pg pa_, pb_;
   load_page(pa_, ch0 + wave);
-  const int half = HD / 2;
-  if (FUSE) {
-    // q heads of this group, and (last split only) this position's k and v
-    const int nqkv = (hq + 2 * hkv) * HD;
-    const size_t rb = (size_t)i * nqkv;
-    for (int e = threadIdx.x; e < G * half; e += 256) {
-      int gh = e / half, cc = e - gh * half;
-      size_t col = (size_t)(g * G + gh) * HD + cc;
-      float a = split_sum(qkv_ws, qkv_splits, qkv_stride, rb + col);
-      float b = split_sum(qkv_ws, qkv_splits, qkv_stride, rb + col + half);
-      float2 cs = rope[(size_t)r.pos * half + cc];
-      q_s[gh][cc] = f32_to_bf16(a * cs.x - b * cs.y);
-      q_s[gh][cc + half] = f32_to_bf16(b * cs.x + a * cs.y);
-    }
-    if (ch1 == nch && threadIdx.x < HD) {
-      const int cc = threadIdx.x;
-      if (cc < half) {
-        size_t col = (size_t)(hq + g) * HD + cc;
-        float a = split_sum(qkv_ws, qkv_splits, qkv_stride, rb + col);
-        float b = split_sum(qkv_ws, qkv_splits, qkv_stride, rb + col + half);
-        float2 cs = rope[(size_t)r.pos * half + cc];
-        kc[kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc, r.pos)] = f32_to_bf16(a * cs.x - b * cs.y);
-        kc[kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc + half, r.pos)] =
-            f32_to_bf16(b * cs.x + a * cs.y);
-      }
-      size_t colv = (size_t)(hq + hkv + g) * HD + cc;
-      vc[vt_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc, r.pos)] =
-          f32_to_bf16(split_sum(qkv_ws, qkv_splits, qkv_stride, rb + colv));
-    }
-    __syncthreads();
-  }
-  // the newest position was appended after the early load of this wave's
-  // first page: reload that page if it is the one holding it
-  if (FUSE && ch1 == nch && ch0 + wave == nch - 1) load_page(pa_, ch0 + wave);
   // q operand: head `row` of this KV group (zero beyond G), dims [DPL*grp, DPL*grp + DPL)
   if (row < G) {
-    const uint4* qp = FUSE ? (const uint4*)(&q_s[row][DPL * grp])
-                           : (const uint4*)(qbuf + ((size_t)i * hq + g * G + row) * HD + DPL * grp);
+    const uint4* qp = (const uint4*)(qbuf + ((size_t)i * hq + g * G + row) * HD + DPL * grp);
 #pragma unroll
     for (int cc = 0; cc < NCC; ++cc) qv[cc] = qp[cc];
   } else {
@@ -893,7 +882,6 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
 #pragma unroll
     for (int q = 0; q < 4; ++q) o_w[wave][4 * grp + q][16 * t + row] = o[t][q];
   __syncthreads();
-  const int ns = (nch + kAttnChunks - 1) / kAttnChunks;
   for (int e = threadIdx.x; e < G * HD; e += 256) {
     int h = e / HD, dd = e - h * HD;
     float mx = fmaxf(fmaxf(m_w[0][h], m_w[1][h]), fmaxf(m_w[2][h], m_w[3][h]));
@@ -904,88 +892,233 @@ __global__ __launch_bounds__(256) void k_attn_mfma(const int32_t* __restrict__ M
       num += wt * o_w[w][h][dd];
       den += wt * l_w[w][h];
     }
-    if (FUSE && ns == 1) {
-      out[((size_t)i * hq + g * G + h) * HD + dd] = f32_to_bf16(num / den);
-    } else {
-      float* dst = part + ((((size_t)i * hkv + g) * n_splits + c) * kMaxGroup + h) * (HD + 2);
-      dst[dd] = num;
-      if (dd == 0) { dst[HD] = mx; dst[HD + 1] = den; }
-    }
+    float* dst = part + ((((size_t)i * hkv + g) * n_splits + c) * kMaxGroup + h) * (HD + 2);
+    dst[dd] = num;
+    if (dd == 0) { dst[HD] = mx; dst[HD + 1] = den; }
   }
   __syncthreads();   // LDS is reused by the next item
   }
 }
 
-// Decode attention (bf16, MFMA), one block per (split c, row i, KV head g)
-// with splits of kDecPages pages.  Every wave owns kDecPpw consecutive pages
-// of the split and issues all of their K and V loads before anything else,
-// so a split costs one HBM round trip; the pages of a small batch spread over
-// several blocks per CU.  The page math is that of k_attn_mfma: S^T = K q^T
-// on v_mfma_f32_16x16x32_bf16, online softmax over the 4 lanes holding a
-// head's 16 scores, O += P V on v_mfma_f32_16x16x16bf16_1k with P as a bf16
-// hi + lo pair.
-//
-// The block also forms its query heads from the fused q|k|v GEMM partials
-// (split sum, rotate-half RoPE, bf16).  The split holding the row's newest
-// position computes that position's k and v, appends them to the row's
-// private KV page, and writes them into the registers of the wave whose page
-// holds the position (the page was loaded before the append).  A row with a
-// single split writes its normalised output straight to `out` ([row][hq][HD],
-// bf16); other rows leave per-split partials for k_attn_combine.
+// Fused q|k|v projection of the decode rows with the rotary / KV-append
+// epilogue (bf16 weights in rotation-pair order, see qkv_pair_col).  Block =
+// one 16-row weight tile; its 4 waves take a quarter of K each and stream
+// their weight fragments and the activation fragments of up to 16*MT rows
+// through a D-stage register pipeline (the waves share no k range, so the
+// activations need no LDS staging).  The wave partial sums meet in LDS and
+// are added in wave order (deterministic).  Wave t % 4 then finishes
+// activation tile t: rotate-half RoPE on q and k heads (the two members of
+// a rotation pair sit in lanes l and l ^ 32), q to qbuf as bf16, k and v to
+// the row's newest KV page (the attention kernel reads them from there).
+template <int HD, int MT, int D, int KS>
+__device__ __forceinline__ void qkv_rope_mblock(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
+    int M, int m_base, int K, f32x4 (*red)[8][64], const RowDesc* __restrict__ rows,
+    const float2* __restrict__ row_rope, int hq, int hkv, int layer, int64_t n_blocks,
+    uint16_t* __restrict__ qbuf, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = lane & 15, grp = lane >> 4;
+  const int tile = blockIdx.x;
+  // KS = K / 128 32-wide k steps per wave; D divides KS, so the pipeline
+  // issues D - 1 surplus (clamped, cache-hit) loads at most, none when D = KS
+  static_assert(KS % D == 0, "pipeline depth must divide the k steps");
+  const int ks0 = wave * KS;
+  const int woff = (tile * (K >> 5) + ks0) * 512 + lane * 8;
+  // activation fragments: X is fragment-major (tiled_index layout, as the
+  // weights), so each fragment load of a wave is one contiguous 1 KiB read;
+  // lanes of rows past M read rows of the last tile whose results are dropped
+  int xoff[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) xoff[t] = ((m_base / 16 + t) * (K >> 5) + ks0) * 512 + lane * 8;
+  // Epilogue inputs of the tiles this wave finishes (t = wave + 4 * tt),
+  // loaded before the k loop so that their latency hides behind it:
+  // the row's newest-token KV slot and the rotation angles of its position.
+  constexpr int TT = (MT + 3) / 4;
+  constexpr int half = HD / 2;
+  const int c0 = tile * 16, h = c0 / HD, jt = (c0 % HD) >> 4;
+  const bool second = grp >= 2;
+  const int dd = 8 * jt + 4 * (grp & 1);           // rotation index of the lane's first dim
+  const int nd = (second ? half : 0) + dd;          // its natural dim within the head
+  size_t pg_e[TT];
+  int on_e[TT];
+  float2 cs_e[TT][4];
+#pragma unroll
+  for (int tt = 0; tt < TT; ++tt) {
+    const int m = min(m_base + 16 * (wave + 4 * tt) + row, M - 1);
+    const RowDesc r = rows[m];
+    const int rel = r.pos - r.plen;                 // private position of the newest token
+    pg_e[tt] = (size_t)layer * n_blocks + r.kv1 + (rel >> 4);
+    on_e[tt] = rel & 15;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) cs_e[tt][q] = row_rope[(size_t)m * half + dd + q];
+  }
+  struct Stage { u32x4 w; u32x4 x[MT]; };
+  Stage st[D];
+  f32x4 acc[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int last = KS - 1;
+  auto load = [&](Stage& sg, int step) {
+    const int kk = max(min(step, last), 0);
+    sg.w = *(const u32x4*)(W + woff + kk * 512);
+#pragma unroll
+    for (int t = 0; t < MT; ++t) sg.x[t] = *(const u32x4*)(X + xoff[t] + kk * 512);
+  };
+  auto consume = [&](Stage& sg, int step) {
+    if (step < KS) {
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, sg.w),
+                                                         __builtin_bit_cast(bf16x8, sg.x[t]), acc[t], 0, 0, 0);
+    }
+  };
+  int base0 = -D;
+  asm volatile("" : "+s"(base0));       // opaque start: the first (load-only) trip stays in the loop
+  for (int base = base0; base < KS; base += D) {
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+      load(st[(j + D - 1) % D], base + j + D - 1);
+      if (base >= 0) consume(st[j], base + j);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < MT; ++t) red[wave][t][lane] = acc[t];
+  __syncthreads();
+#pragma unroll
+  for (int tt = 0; tt < TT; ++tt) {
+    const int t = wave + 4 * tt;
+    if (t >= MT) break;
+    f32x4 v = red[0][t][lane];
+    v += red[1][t][lane];
+    v += red[2][t][lane];
+    v += red[3][t][lane];
+    f32x4 pv;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) pv[q] = __shfl_xor(v[q], 32, 64);
+    const int m = m_base + 16 * t + row;
+    if (m >= M) continue;
+    float o[4];
+    if (h < hq + hkv) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float2 c = cs_e[tt][q];
+        o[q] = second ? (v[q] * c.x + pv[q] * c.y) : (v[q] * c.x - pv[q] * c.y);
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = v[q];
+    }
+    const uint32_t p01 = (uint32_t)f32_to_bf16(o[0]) | ((uint32_t)f32_to_bf16(o[1]) << 16);
+    const uint32_t p23 = (uint32_t)f32_to_bf16(o[2]) | ((uint32_t)f32_to_bf16(o[3]) << 16);
+    const size_t pg = pg_e[tt];
+    const int on = on_e[tt];
+    if (h < hq) {
+      *(uint2*)(qbuf + ((size_t)m * hq + h) * HD + nd) = make_uint2(p01, p23);
+    } else if (h < hq + hkv) {
+      *(uint2*)(kc + ((pg * hkv + (h - hq)) * kBlockTok + on) * HD + nd) = make_uint2(p01, p23);
+    } else {
+      uint16_t* vp = vc + (pg * hkv + (h - hq - hkv)) * (size_t)HD * kBlockTok + on;
+      vp[(size_t)(nd + 0) * kBlockTok] = (uint16_t)(p01 & 0xFFFF);
+      vp[(size_t)(nd + 1) * kBlockTok] = (uint16_t)(p01 >> 16);
+      vp[(size_t)(nd + 2) * kBlockTok] = (uint16_t)(p23 & 0xFFFF);
+      vp[(size_t)(nd + 3) * kBlockTok] = (uint16_t)(p23 >> 16);
+    }
+  }
+  __syncthreads();   // red is reused by the next m-block
+}
+
+// Live row count read on the device; m-blocks of up to 128 rows, each with
+// just enough 16-row activation tiles.  Grid: one block per weight tile.
+// KS = d_model / 128, one of 4, 8, 12, 16, 24, 32 (checked by sara_init).
+template <int HD, int KS>
+__global__ __launch_bounds__(256) void k_qkv_rope(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
+    const int32_t* __restrict__ M_ptr, int K, const RowDesc* __restrict__ rows,
+    const float2* __restrict__ row_rope, int hq, int hkv, int layer, int64_t n_blocks,
+    uint16_t* __restrict__ qbuf, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
+  __shared__ f32x4 red[4][8][64];
+  const int M = *M_ptr;
+  for (int m_base = 0; m_base < M; m_base += 128) {
+    const int mt = min(8, (M - m_base + 15) >> 4);
+    // depth: every k step (at most 16) in flight for up to 32 rows, then a half and a quarter
+#define SARA_QR(MT_, D_) \
+    if (mt == MT_) qkv_rope_mblock<HD, MT_, D_, KS>(X, W, M, m_base, K, red, rows, row_rope, hq, hkv, layer, \
+                                                    n_blocks, qbuf, kc, vc);
+    constexpr int D1 = KS <= 16 ? KS : KS / 2, D3 = D1 / 2, D5 = D1 / 4;
+    SARA_QR(1, D1) SARA_QR(2, D1) SARA_QR(3, D3) SARA_QR(4, D3)
+    SARA_QR(5, D5) SARA_QR(6, D5) SARA_QR(7, D5) SARA_QR(8, D5)
+#undef SARA_QR
+  }
+}
+
+// Decode attention (bf16, MFMA) over the KV pages, q read from qbuf (the
+// q|k|v kernel has already rotated q and appended this position's k and v).
+// Item = (split c, row i, KV head g), split-major; a split is kDecPages
+// pages and wave w owns pages w, w + 4, .. of it, all K and V loads issued
+// before any compute, so a split costs one HBM round trip.  Page ids come
+// from the row's two KV extents (kv0 + e: shared prompt pages, kv1 + e:
+// private pages), so no block-table read sits between the row descriptor
+// and the page loads.  Per page (16 tokens):
+//   S^T = K q^T  (v_mfma_f32_16x16x32_bf16; G <= 8 query heads padded to 16;
+//                 lane (token l%16, k-group l/16) of K meets head l%16 of q
+//                 over the same HD/4 dims, so the k order inside the MFMA is moot)
+//   online softmax per head over the 4 lanes holding its 16 scores
+//   O += P V     (v_mfma_f32_16x16x16bf16_1k; the score registers already
+//                 have the A-operand layout and transposed V pages give the
+//                 B operand; P enters as a bf16 hi + lo pair, so the product
+//                 keeps fp32 accuracy without a bf16 rounding point)
+// The 4 waves' (max, sum, O) merge in LDS.  A row with a single split writes
+// its normalised output to `out` ([row][hq][HD], bf16); other rows leave a
+// partial per split for k_attn_combine.
 template <int HD>
-__global__ __launch_bounds__(256) void k_attn_dec(const int32_t* __restrict__ M_ptr,
-    const RowDesc* __restrict__ rows, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
-    const int32_t* __restrict__ btab, int MAXB, int PB, int layer, int64_t n_blocks, int hq,
-    int hkv, int n_splits, float scale, float* __restrict__ part,
-    const float* __restrict__ qkv_ws, int qkv_splits, int64_t qkv_stride,
-    const float2* __restrict__ rope, uint16_t* __restrict__ out) {
+__global__ __launch_bounds__(256, 2) void k_attn_dec(const int32_t* __restrict__ M_ptr,
+    const RowDesc* __restrict__ rows, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+    int layer, int64_t n_blocks, int hq, int hkv, int n_splits, float scale,
+    const uint16_t* __restrict__ qb, float* __restrict__ part, uint16_t* __restrict__ out) {
   typedef short short4_ __attribute__((ext_vector_type(4)));
   typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-  constexpr int DPL = HD / 4;     // dims per lane in the QK^T operands
-  constexpr int NCC = HD / 32;    // 16x16x32 MFMAs per page for QK^T
-  constexpr int NT = HD / 16;     // output tiles of 16 dims
-  constexpr int PPW = kDecPpw;
+  constexpr int DPL = HD / 4, NCC = HD / 32, NT = HD / 16, PPW = kDecPpw, SPG = kDecPages;
   __shared__ float m_w[4][16], l_w[4][16];
   __shared__ float o_w[4][16][HD + 1];
-  __shared__ __attribute__((aligned(16))) uint16_t q_s[kMaxGroup][HD];
-  __shared__ __attribute__((aligned(16))) uint16_t kn_s[HD];
-  __shared__ uint16_t vn_s[HD];
   const int M = *M_ptr;
   const int total = M * hkv * n_splits;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = lane & 15, grp = lane >> 4;
   const int G = hq / hkv;
-  const int half = HD / 2;
   for (int item = blockIdx.x; item < total; item += gridDim.x) {
     const int c = item / (M * hkv);
     const int i = (item - c * M * hkv) / hkv, g = item % hkv;
+    // q operand (head `row` of this KV group, zero beyond G): independent of
+    // the row descriptor, loaded first
+    uint4 qv[NCC];
+    {
+      const int hh = min(row, G - 1);
+      const uint4* qp = (const uint4*)(qb + ((size_t)i * hq + g * G + hh) * HD + DPL * grp);
+#pragma unroll
+      for (int cc = 0; cc < NCC; ++cc) qv[cc] = qp[cc];
+      if (row >= G) {
+#pragma unroll
+        for (int cc = 0; cc < NCC; ++cc) qv[cc] = make_uint4(0, 0, 0, 0);
+      }
+    }
     const RowDesc r = rows[i];
     const int ctx = r.pos + 1;
     const int pl = min(ctx, r.plen);                      // prompt positions attended
     const int pc = (pl + 15) >> 4;                         // prompt pages
     const int vcnt = ctx - pl;                             // private positions (>= 1)
     const int nch = pc + ((vcnt + 15) >> 4);
-    const int ch0 = c * kDecPages;
+    const int ch0 = c * SPG;
     if (ch0 >= nch) continue;
-    const int ch1 = min(nch, ch0 + kDecPages);
-    const bool has_new = (ch1 == nch);
-    const int32_t* bt = btab + (size_t)r.tab * MAXB;
-    int my_blk = 0;
-    if (lane < kDecPages && ch0 + lane < ch1) {
-      const int cl = ch0 + lane;
-      my_blk = bt[(cl < pc) ? cl : PB + (cl - pc)];
-    }
+    const int ch1 = min(nch, ch0 + SPG);
     struct Pg { u32x4 k[NCC]; u32x2 v[NT]; int n; };
     Pg pg[PPW];
 #pragma unroll
     for (int p = 0; p < PPW; ++p) {
-      const int ch = ch0 + wave * PPW + p;
+      const int ch = ch0 + wave + 4 * p;
       const int cv = (ch < ch1) ? ch : ch0;                // pages past the split re-read its first
       int n;
       if (cv < pc) n = min(16, pl - 16 * cv);
       else n = min(16, vcnt - 16 * (cv - pc));
       pg[p].n = (ch < ch1) ? n : 0;
-      const int blk = __shfl(my_blk, cv - ch0, 64);
+      const int blk = (cv < pc) ? r.kv0 + cv : r.kv1 + (cv - pc);
       const size_t pgi = ((size_t)layer * n_blocks + blk) * hkv + g;
       const u32x4* kp = (const u32x4*)(kc + (pgi * kBlockTok + row) * HD + DPL * grp);
 #pragma unroll
@@ -993,96 +1126,6 @@ __global__ __launch_bounds__(256) void k_attn_dec(const int32_t* __restrict__ M_
       const uint16_t* vp = vc + pgi * (size_t)HD * kBlockTok + 4 * grp;
 #pragma unroll
       for (int t = 0; t < NT; ++t) pg[p].v[t] = *(const u32x2*)(vp + (size_t)(16 * t + row) * kBlockTok);
-    }
-    // query heads of this KV group, then the newest position's k and v:
-    // rotation pairs (dim cc, cc + HD/2); the G*HD/2 query pairs and (last
-    // split) the HD/2 key pairs and HD value dims are spread over the
-    // threads, kPairsPT per thread, all partial loads issued together
-    const size_t rb = (size_t)i * (size_t)((hq + 2 * hkv) * HD);
-    const int nq = G * half, nk = has_new ? half : 0, nv = has_new ? HD : 0;
-    {
-      constexpr int PT = (kMaxGroup * HD / 2 + HD / 2 + HD + 255) / 256;
-      float va[PT], vb[PT];
-      float2 cs[PT];
-#pragma unroll
-      for (int t = 0; t < PT; ++t) {
-        // column indices first (always valid), then unconditional loads
-        const int e = threadIdx.x + 256 * t;
-        int ca = 0, rp = 0;
-        if (e < nq) {
-          const int gh = e / half, cc = e - gh * half;
-          ca = (g * G + gh) * HD + cc;
-          rp = cc;
-        } else if (e < nq + nk) {
-          const int cc = e - nq;
-          ca = (hq + g) * HD + cc;
-          rp = cc;
-        } else if (e < nq + nk + nv) {
-          ca = (hq + hkv + g) * HD + (e - nq - nk);
-        }
-        const int cb = (e < nq + nk) ? ca + half : ca;
-        va[t] = split_sum8(qkv_ws, qkv_splits, qkv_stride, rb + ca);
-        vb[t] = split_sum8(qkv_ws, qkv_splits, qkv_stride, rb + cb);
-        cs[t] = rope[(size_t)r.pos * half + rp];
-      }
-#pragma unroll
-      for (int t = 0; t < PT; ++t) {
-        const int e = threadIdx.x + 256 * t;
-        const float a = va[t], b = vb[t];
-        const uint16_t r0 = f32_to_bf16(a * cs[t].x - b * cs[t].y), r1 = f32_to_bf16(b * cs[t].x + a * cs[t].y);
-        if (e < nq) {
-          const int gh = e / half, cc = e - gh * half;
-          q_s[gh][cc] = r0;
-          q_s[gh][cc + half] = r1;
-        } else if (e < nq + nk) {
-          const int cc = e - nq;
-          kn_s[cc] = r0;
-          kn_s[cc + half] = r1;
-          kc[kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc, r.pos)] = r0;
-          kc[kv_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc + half, r.pos)] = r1;
-        } else if (e < nq + nk + nv) {
-          const int cc = e - nq - nk;
-          const uint16_t v0 = f32_to_bf16(a);
-          vn_s[cc] = v0;
-          vc[vt_index(r, btab, MAXB, PB, layer, n_blocks, hkv, g, HD, cc, r.pos)] = v0;
-        }
-      }
-    }
-    __syncthreads();
-    if (has_new) {
-      // the newest position is private token o_new of page nch - 1
-      const int rel = nch - 1 - ch0;
-      const int o_new = (vcnt - 1) & 15;
-      if (rel / PPW == wave) {
-#pragma unroll
-        for (int p = 0; p < PPW; ++p) {
-          if (p != rel % PPW) continue;
-          if (row == o_new) {
-#pragma unroll
-            for (int cc = 0; cc < NCC; ++cc) pg[p].k[cc] = *(const u32x4*)&kn_s[DPL * grp + 8 * cc];
-          }
-          if ((o_new >> 2) == grp) {
-            const int q = o_new & 3;
-#pragma unroll
-            for (int t = 0; t < NT; ++t) {
-              const uint32_t nv = vn_s[16 * t + row];
-              uint32_t w = (q < 2) ? pg[p].v[t].x : pg[p].v[t].y;
-              w = (q & 1) ? ((w & 0x0000FFFFu) | (nv << 16)) : ((w & 0xFFFF0000u) | nv);
-              if (q < 2) pg[p].v[t].x = w; else pg[p].v[t].y = w;
-            }
-          }
-        }
-      }
-    }
-    // q operand: head `row` of this KV group (zero beyond G), dims [DPL*grp, DPL*grp + DPL)
-    uint4 qv[NCC];
-    if (row < G) {
-      const uint4* qp = (const uint4*)(&q_s[row][DPL * grp]);
-#pragma unroll
-      for (int cc = 0; cc < NCC; ++cc) qv[cc] = qp[cc];
-    } else {
-#pragma unroll
-      for (int cc = 0; cc < NCC; ++cc) qv[cc] = make_uint4(0, 0, 0, 0);
     }
     float m_run = -INFINITY, l_run = 0.f;
     f32x4 o[NT];
@@ -1123,6 +1166,7 @@ __global__ __launch_bounds__(256) void k_attn_dec(const int32_t* __restrict__ M_
       ps += __shfl_xor(ps, 32, 64);
       l_run = l_run * alpha + ps;
       m_run = mn;
+      // rows of O are heads 4*grp + q: fetch their rescale factors
       float al[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) al[q] = __shfl(alpha, 4 * grp + q, 64);
@@ -1136,8 +1180,8 @@ __global__ __launch_bounds__(256) void k_attn_dec(const int32_t* __restrict__ M_
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const uint32_t w = (q < 2) ? pg[p].v[t].x : pg[p].v[t].y;
-          const uint16_t h = (uint16_t)((q & 1) ? (w >> 16) : (w & 0xFFFF));
-          vb[q] = (short)((4 * grp + q < n) ? h : (uint16_t)0);
+          const uint16_t hv = (uint16_t)((q & 1) ? (w >> 16) : (w & 0xFFFF));
+          vb[q] = (short)((4 * grp + q < n) ? hv : (uint16_t)0);
         }
 #pragma unroll
         for (int q = 0; q < 4; ++q) o[t][q] *= al[q];
@@ -1152,21 +1196,21 @@ __global__ __launch_bounds__(256) void k_attn_dec(const int32_t* __restrict__ M_
 #pragma unroll
       for (int q = 0; q < 4; ++q) o_w[wave][4 * grp + q][16 * t + row] = o[t][q];
     __syncthreads();
-    const int ns = (nch + kDecPages - 1) / kDecPages;
+    const int ns = (nch + SPG - 1) / SPG;
     for (int e = threadIdx.x; e < G * HD; e += 256) {
-      const int h = e / HD, dd = e - h * HD;
-      const float mx = fmaxf(fmaxf(m_w[0][h], m_w[1][h]), fmaxf(m_w[2][h], m_w[3][h]));
+      const int hh = e / HD, dd = e - hh * HD;
+      const float mx = fmaxf(fmaxf(m_w[0][hh], m_w[1][hh]), fmaxf(m_w[2][hh], m_w[3][hh]));
       float num = 0.f, den = 0.f;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        const float wt = (m_w[w][h] == -INFINITY) ? 0.f : expf(m_w[w][h] - mx);
-        num += wt * o_w[w][h][dd];
-        den += wt * l_w[w][h];
+        const float wt = (m_w[w][hh] == -INFINITY) ? 0.f : expf(m_w[w][hh] - mx);
+        num += wt * o_w[w][hh][dd];
+        den += wt * l_w[w][hh];
       }
       if (ns == 1) {
-        out[((size_t)i * hq + g * G + h) * HD + dd] = f32_to_bf16(num / den);
+        out[((size_t)i * hq + g * G + hh) * HD + dd] = f32_to_bf16(num / den);
       } else {
-        float* dst = part + ((((size_t)i * hkv + g) * n_splits + c) * kMaxGroup + h) * (HD + 2);
+        float* dst = part + ((((size_t)i * hkv + g) * n_splits + c) * kMaxGroup + hh) * (HD + 2);
         dst[dd] = num;
         if (dd == 0) { dst[HD] = mx; dst[HD + 1] = den; }
       }
@@ -1474,13 +1518,13 @@ static int attn_grid(sara_ctx* c, int M_cap) {
 
 // h += split-K sum of ws; x = RMSNorm(h) * w
 template <typename T>
-static void residual_norm(sara_ctx* c, const int32_t* M_ptr, int M_cap, int sp, const float* w) {
+static void residual_norm(sara_ctx* c, const int32_t* M_ptr, int M_cap, int sp, const float* w, int x_tiled = 0) {
   const int d = c->d, vpt = (d + 255) / 256;
   const dim3 grid(std::min(M_cap, 1024));
   const int64_t stride = (int64_t)M_cap * d;
   T* x = (T*)c->x;
 #define SARA_RN(V) hipLaunchKernelGGL((k_residual_norm_v<T, V>), grid, dim3(256), 0, c->stream, M_ptr, c->ws, \
-                                      sp, stride, d, c->h, w, c->md.rms_eps, x)
+                                      sp, stride, d, c->h, w, c->md.rms_eps, x, x_tiled)
   switch (sp <= kMaxSplitsDec ? vpt : 0) {
     case 1: SARA_RN(1); break;
     case 2: SARA_RN(2); break;
@@ -1490,7 +1534,7 @@ static void residual_norm(sara_ctx* c, const int32_t* M_ptr, int M_cap, int sp, 
     case 7: case 8: SARA_RN(8); break;
     default:
       hipLaunchKernelGGL(k_residual_norm<T>, dim3(std::min(M_cap, 256)), dim3(1024), 0, c->stream, M_ptr,
-                         c->ws, sp, stride, d, c->h, w, c->md.rms_eps, x);
+                         c->ws, sp, stride, d, c->h, w, c->md.rms_eps, x, x_tiled);
   }
 #undef SARA_RN
 }
@@ -1502,20 +1546,31 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
   const int64_t stride_qkv = (int64_t)M_cap * c->nqkv;
   T* x = (T*)c->x;
   for (int l = 0; l < c->L; ++l) {
-    int sp;
-    PROF_B(c);
-    gemm(c, x, c->w_qkv[l], M_ptr, M_cap, c->nqkv, d, sp);
-    PROF_E(c, kPGemmN1, c->nqkv, d);
+    int sp = 1;
     const bool mfma_attn = (c->md.dtype == SARA_BF16);
     if (mfma_attn && !c->in_prefill) {
-      // decode: q|k|v epilogue and attention in one kernel, then the split merge
+      // decode: q|k|v projection with the RoPE / KV-append epilogue, the
+      // paged attention, then the merge of rows with several context splits
+      PROF_B(c);
+#define SARA_QKV(KS_) \
+      hipLaunchKernelGGL((k_qkv_rope<HD, KS_>), dim3(c->nqkv / 16), dim3(256), 0, st, (const uint16_t*)x, \
+                         (const uint16_t*)c->w_qkv[l], M_ptr, d, c->rows, c->row_rope, c->hq, c->hkv, l, \
+                         c->n_blocks, (uint16_t*)c->qbuf, (uint16_t*)c->kc, (uint16_t*)c->vc)
+      switch (d / 128) {
+        case 4: SARA_QKV(4); break;
+        case 8: SARA_QKV(8); break;
+        case 12: SARA_QKV(12); break;
+        case 16: SARA_QKV(16); break;
+        case 24: SARA_QKV(24); break;
+        default: SARA_QKV(32); break;
+      }
+#undef SARA_QKV
+      PROF_E(c, kPQkvRope, c->nqkv, d);
       PROF_B(c);
       const int dg = (int)std::min<int64_t>((int64_t)M_cap * c->hkv * c->dec_splits_max, 2048);
-      hipLaunchKernelGGL((k_attn_dec<HD>), dim3(dg), dim3(256), 0, st,
-                         M_ptr, c->rows, (uint16_t*)c->kc, (uint16_t*)c->vc, c->btab,
-                         c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv, c->dec_splits_max,
-                         1.0f / sqrtf((float)HD), c->attn_part, (const float*)c->ws, sp, stride_qkv, c->rope,
-                         (uint16_t*)x);
+      hipLaunchKernelGGL((k_attn_dec<HD>), dim3(dg), dim3(256), 0, st, M_ptr, c->rows, (const uint16_t*)c->kc,
+                         (const uint16_t*)c->vc, l, c->n_blocks, c->hq, c->hkv, c->dec_splits_max,
+                         1.0f / sqrtf((float)HD), (const uint16_t*)c->qbuf, c->attn_part, (uint16_t*)x);
       PROF_E(c, kPAttn, 0, 0);
       PROF_B(c);
       hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(1024), dim3(HD), 0, st, M_ptr, c->rows,
@@ -1523,18 +1578,20 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
       PROF_E(c, kPCombine, 0, 0);
     } else {
     PROF_B(c);
+    gemm(c, x, c->w_qkv[l], M_ptr, M_cap, c->nqkv, d, sp);
+    PROF_E(c, kPGemmN1, c->nqkv, d);
+    PROF_B(c);
     hipLaunchKernelGGL(k_qkv_epilogue<T>, dim3(2048), dim3(c->hd / 2), 0, st, M_ptr,
                        c->rows, c->ws, sp,
                        stride_qkv, c->rope, c->hq, c->hkv, c->hd, l, c->n_blocks, c->btab, c->MAXB,
-                       c->PB, (T*)c->qbuf, (T*)c->kc, (T*)c->vc);
+                       c->PB, (T*)c->qbuf, (T*)c->kc, (T*)c->vc, mfma_attn ? 1 : 0);
     PROF_E(c, kPQkv, c->nqkv, 0);
     PROF_B(c);
     if (mfma_attn)
-      hipLaunchKernelGGL((k_attn_mfma<HD, 0>), dim3(attn_grid(c, M_cap)), dim3(256), 0, st,
-                         M_ptr, c->rows, (const uint16_t*)c->qbuf, (uint16_t*)c->kc,
-                         (uint16_t*)c->vc, c->btab, c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv,
-                         c->attn_splits_max, 1.0f / sqrtf((float)HD), c->attn_part, (const float*)nullptr, 0,
-                         (int64_t)0, c->rope, (uint16_t*)nullptr);
+      hipLaunchKernelGGL((k_attn_mfma<HD>), dim3(attn_grid(c, M_cap)), dim3(256), 0, st,
+                         M_ptr, c->rows, (const uint16_t*)c->qbuf, (const uint16_t*)c->kc,
+                         (const uint16_t*)c->vc, c->btab, c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv,
+                         c->attn_splits_max, 1.0f / sqrtf((float)HD), c->attn_part);
     else
       hipLaunchKernelGGL((k_attention<T, HD>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
                          M_ptr, c->rows, (const T*)c->qbuf, (const T*)c->kc, (const T*)c->vc, c->btab,
@@ -1576,7 +1633,9 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     // the last layer's norm output is only needed when logits follow
     if (l + 1 < c->L || final_norm_out) {
       PROF_B(c);
-      residual_norm<T>(c, M_ptr, M_cap, sp, nw);
+      // in bf16 decode the next layer's q|k|v kernel reads fragment-major rows
+      residual_norm<T>(c, M_ptr, M_cap, sp, nw,
+                       (c->md.dtype == SARA_BF16 && !c->in_prefill && l + 1 < c->L) ? 1 : 0);
       PROF_E(c, kPResNorm, d, 0);
     }
   }
@@ -1598,7 +1657,7 @@ int launch_prefill(sara_ctx* c) {
   for (int64_t r0 = 0; r0 < rows_total; r0 += c->prefill_rows) {
     int n = (int)((rows_total - r0 < c->prefill_rows) ? rows_total - r0 : c->prefill_rows);
     hipLaunchKernelGGL(k_prefill_rows, dim3((n + 255) / 256), dim3(256), 0, st, c->pre, c->U, (int)r0,
-                       n, c->tok, c->off, c->S, c->rows, c->rows_M);
+                       n, c->tok, c->off, c->S, c->rows, c->rows_M, c->PB);
     if (c->md.dtype == SARA_BF16) {
       hipLaunchKernelGGL(k_embed_norm<uint16_t>, dim3(n), dim3(256), 0, st, c->rows_M, c->rows,
                          (const uint16_t*)c->embed, c->norms, c->d, c->md.rms_eps, c->h,
@@ -1623,12 +1682,14 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
     hipLaunchKernelGGL(k_decode_embed<uint16_t>, dim3(eg), dim3(256), 0, st, c->ctl, c->active, c->slot_uid,
                        c->slot_j, c->slot_gen, c->tok, c->off, c->out_tok, c->k, c->ad.max_new, c->rows,
                        c->rows_M, model_free ? 0 : 1, (const uint16_t*)c->embed, c->norms, c->d,
-                       c->md.rms_eps, c->h, (uint16_t*)c->x);
+                       c->md.rms_eps, c->h, (uint16_t*)c->x, c->U, c->PB, c->SB, c->rope, c->hd / 2,
+                       c->row_rope, 1);
   else
     hipLaunchKernelGGL(k_decode_embed<float>, dim3(eg), dim3(256), 0, st, c->ctl, c->active, c->slot_uid,
                        c->slot_j, c->slot_gen, c->tok, c->off, c->out_tok, c->k, c->ad.max_new, c->rows,
                        c->rows_M, model_free ? 0 : 1, (const float*)c->embed, c->norms, c->d,
-                       c->md.rms_eps, c->h, (float*)c->x);
+                       c->md.rms_eps, c->h, (float*)c->x, c->U, c->PB, c->SB, c->rope, c->hd / 2,
+                       c->row_rope, 0);
   PROF_E(c, kPEmbed, c->d, 0);
   if (!model_free) {
     if (c->md.dtype == SARA_BF16) layers<uint16_t>(c, c->rows_M, S, true);
@@ -1692,6 +1753,14 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
 int launch_tile_weights(sara_ctx* c, const void* src, void* dst, int rows, int K, int tile_mul, int tile_add) {
   hipLaunchKernelGGL(k_tile_weights, dim3(2048), dim3(256), 0, c->stream, (const uint16_t*)src, (uint16_t*)dst,
                      rows / 16, K, tile_mul, tile_add);
+  return SARA_OK;
+}
+
+// Rows of heads head_off.. of a q, k or v weight ([n_rows][K], natural
+// order) into the fused q|k|v tiles in rotation-pair order.
+int launch_tile_weights_pairs(sara_ctx* c, const void* src, void* dst, int n_rows, int K, int head_off) {
+  hipLaunchKernelGGL(k_tile_weights_pairs, dim3(2048), dim3(256), 0, c->stream, (const uint16_t*)src,
+                     (uint16_t*)dst, n_rows, K, head_off, c->hd);
   return SARA_OK;
 }
 

@@ -36,7 +36,7 @@ static int einval(const std::string& msg) {
 const char* const kProfNames[kPNumClasses] = {
     "k_gemm_bf16_lds<1,8,64,0,0>", "k_gemm_bf16_lds<2,8,64,1,0>", "k_gemm_bf16_lds<2,8,64,0,0>",
     "k_attn_mfma<128>", "k_attn_combine", "k_qkv_epilogue", "k_residual_norm", "k_swiglu",
-    "k_embed_norm", "k_sample_partial", "k_sample_final", "k_decode_rows", "k_copy_logits",
+    "k_embed_norm", "k_sample_partial", "k_sample_final", "k_decode_rows", "k_copy_logits", "k_qkv_rope",
     ".gemm[q|k|v]", ".gemm[o]", ".gemm[gate|up]", ".gemm[down]", ".gemm[lm_head]"};
 
 void prof_begin(sara_ctx* c) {
@@ -82,6 +82,8 @@ int prof_collect(sara_ctx* c) {
         break;
       case kPCombine: by = m * c->qdim * (4.0 + E); break;
       case kPQkv: by = m * N * (4.0 + E); break;
+      case kPQkvRope:   // fused q|k|v weights, normed input rows, q and the appended k, v
+        by = N * K * E + m * K * E + m * N * E; fl = 2.0 * m * N * K; break;
       case kPResNorm: by = m * N * (12.0 + E); break;
       case kPSwiglu: by = m * N * (8.0 + E); break;
       case kPEmbed: by = m * N * (2.0 * E + 4.0); break;
@@ -97,7 +99,7 @@ int prof_collect(sara_ctx* c) {
       t.flops += fl;
     };
     add(r.cls);
-    if (r.cls == kPGemmN1 || r.cls == kPGemmGU || r.cls == kPGemmLM) {
+    if (r.cls == kPGemmN1 || r.cls == kPGemmGU || r.cls == kPGemmLM || r.cls == kPQkvRope) {
       if (r.N == c->V) add(kPGemmLm);
       else if (r.N == c->nqkv) add(kPGemmQkv);
       else if (r.N == 2 * c->ffn) add(kPGemmGu);
@@ -147,6 +149,11 @@ static int validate(const sara_model_desc* m, const sara_alloc_desc* a) {
     return einval("n_heads must be a multiple of n_kv_heads with at most 8 query heads per KV head");
   if (m->d_model % 64 || m->d_ffn % 64 || (m->n_heads * m->head_dim) % 64)
     return einval("d_model, d_ffn and n_heads*head_dim must be multiples of 64");
+  if (m->dtype == SARA_BF16) {
+    const int ks = m->d_model / 128;
+    if (m->d_model % 128 || !(ks == 4 || ks == 8 || ks == 12 || ks == 16 || ks == 24 || ks == 32))
+      return einval("bf16 models need d_model in {512, 1024, 1536, 2048, 3072, 4096}");
+  }
   if (m->dtype == SARA_BF16 && m->d_ffn % 16) return einval("d_ffn must be a multiple of 16");
   if (m->vocab % 16) return einval("vocab must be a multiple of 16");
   if (m->eos_id < -1 || m->eos_id >= m->vocab) return einval("eos_id out of range");
@@ -236,6 +243,7 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   ALLOC(c->vc, kv_bytes);
   ALLOC(c->btab, sizeof(int32_t) * (size_t)(c->S + c->U) * c->MAXB);
   ALLOC(c->rope, sizeof(float2) * (size_t)c->max_pos * (c->hd / 2));
+  ALLOC(c->row_rope, sizeof(float2) * (size_t)c->S * (c->hd / 2));
   // prompt pool
   c->tok_cap = (int64_t)c->U * ad->max_prompt;
   ALLOC(c->tok, sizeof(int32_t) * c->tok_cap);
@@ -307,9 +315,10 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
     const int kvr = c->hkv * c->hd;
     for (int l = 0; l < c->L && e == hipSuccess; ++l) {
       const void* const* w = d_weights + 1 + 9 * l;
-      launch_tile_weights(c, w[1], c->w_qkv[l], c->qdim, d, 1, 0);
-      launch_tile_weights(c, w[2], c->w_qkv[l], kvr, d, 1, c->qdim / 16);
-      launch_tile_weights(c, w[3], c->w_qkv[l], kvr, d, 1, (c->qdim + kvr) / 16);
+      // q|k|v rows fused, each head in rotation-pair order (see qkv_pair_col)
+      launch_tile_weights_pairs(c, w[1], c->w_qkv[l], c->qdim, d, 0);
+      launch_tile_weights_pairs(c, w[2], c->w_qkv[l], kvr, d, c->hq);
+      launch_tile_weights_pairs(c, w[3], c->w_qkv[l], kvr, d, c->hq + c->hkv);
       launch_tile_weights(c, w[4], c->w_o[l], d, c->qdim, 1, 0);
       // gate and up tiles interleaved (gate tile j -> 2j, up tile j -> 2j + 1) for the SwiGLU epilogue
       launch_tile_weights(c, w[6], c->w_gu[l], c->ffn, d, 2, 0);

@@ -49,6 +49,11 @@ struct RowDesc {
   int32_t rid;      // decode: rollout id uid*k + j
   int32_t gen;      // decode: generated index i
   int32_t uid;
+  // KV extents: page ids of a sequence are kv0 + e for its shared prompt
+  // segment (entries e < PB of its block-table row) and kv1 + e for its
+  // private segment (decode rows; -1 for prefill rows)
+  int32_t kv0;
+  int32_t kv1;
 };
 
 // Parameters every controller kernel reads.
@@ -94,6 +99,7 @@ struct sara_ctx {
   void* vc = nullptr;
   int32_t* btab = nullptr;
   float2* rope = nullptr;         // [max_pos][hd/2] (cos, sin)
+  float2* row_rope = nullptr;     // [S][hd/2] (cos, sin) at each decode row's position
 
   // prompt pool (library copies)
   int32_t* tok = nullptr;
@@ -165,7 +171,7 @@ namespace sara {
 // one class per kernel (per template instance for the GEMMs, as a kernel
 // trace names them), then a breakdown of the GEMMs by weight matrix
 enum ProfClass { kPGemmN1, kPGemmGU, kPGemmLM, kPAttn, kPCombine, kPQkv, kPResNorm, kPSwiglu,
-                 kPEmbed, kPSampleP, kPSampleF, kPRows, kPCopy,
+                 kPEmbed, kPSampleP, kPSampleF, kPRows, kPCopy, kPQkvRope,
                  kPGemmQkv, kPGemmO, kPGemmGu, kPGemmD, kPGemmLm, kPNumClasses };
 extern const char* const kProfNames[kPNumClasses];
 void prof_begin(sara_ctx* c);
@@ -192,6 +198,7 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
                        uint32_t feos, int32_t* tok, hipStream_t st);
 int launch_convert_norms(sara_ctx* c, const void* const* w);
 int launch_tile_weights(sara_ctx* c, const void* src, void* dst, int rows, int K, int tile_mul, int tile_add);
+int launch_tile_weights_pairs(sara_ctx* c, const void* src, void* dst, int n_rows, int K, int head_off);
 
 // ---------------------------------------------------------------------------
 // device helpers
