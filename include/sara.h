@@ -217,6 +217,17 @@ int sara_sample_logits(const float* d_logits, int32_t n_rows, int32_t vocab,
                        int32_t step_index, float temperature, int32_t eos_id,
                        uint32_t forced_eos_u32, int32_t* d_tok, void* stream);
 
+/* Self-check of the fused LM-head sampler (bf16 models).  That sampler
+ * scores every vocabulary id with an fp32 estimate of the Gumbel noise and
+ * re-scores exactly (fp64 noise rounded to fp32, the definition of the noise
+ * above) only the ids whose estimate lies within a fixed margin of the best;
+ * its output equals the exact Gumbel-max provided the estimate is within
+ * 2e-5 of the exact noise for every input.  This call evaluates both for all
+ * 2^24 noise inputs on the device and writes the largest absolute distance
+ * to *h_out (host).  Synchronous on stream; returns SARA_EHIP on HIP
+ * failure. */
+int sara_gumbel_fast_max_error(double* h_out, void* stream);
+
 /* Per-kernel timing of eager decode steps.  While enabled, every
  * sara_decode_step call (not the graph replays of sara_run) records a HIP
  * event pair around each kernel it launches on the context's stream, waits

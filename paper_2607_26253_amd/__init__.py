@@ -23,7 +23,8 @@ SARA_COMMIT, SARA_ABANDON, SARA_CONTINUE = 1, 2, 3
 EXPORTED = ["sara_init", "sara_begin_step", "sara_decode_step", "sara_posterior_decide",
             "sara_refill", "sara_run", "sara_query", "sara_finish_step", "sara_read_rollouts",
             "sara_read_logs", "sara_read_advantages", "sara_peff_batch", "grpo_group_advantages",
-            "sara_sample_logits", "sara_set_profiling", "sara_reset_profile", "sara_read_profile",
+            "sara_sample_logits", "sara_gumbel_fast_max_error", "sara_set_profiling", "sara_reset_profile",
+            "sara_read_profile",
             "sara_destroy",
             "sara_last_error"]
 
@@ -79,6 +80,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "sara_peff_batch": [P, P, I32, F64, F64, I32, P, P],
         "grpo_group_advantages": [P, P, I32, F32, P, P],
         "sara_sample_logits": [P, I32, I32, P, P, U64, I32, F32, I32, ctypes.c_uint32, P, P],
+        "sara_gumbel_fast_max_error": [ctypes.POINTER(F64), P],
         "sara_set_profiling": [P, I32],
         "sara_reset_profile": [P],
         "sara_read_profile": [P, ctypes.POINTER(sara_kernel_profile), I32, ctypes.POINTER(I32)],
@@ -293,6 +295,13 @@ def sara_peff_batch(d_n, d_s, k, alpha0, beta0, d_out, stream=None):
 def grpo_group_advantages(d_r, d_group_off, eps, d_adv, stream=None):
     _check(_lib.grpo_group_advantages(_ptr(d_r), _ptr(d_group_off), int(d_group_off.numel()) - 1, float(eps),
                                       _ptr(d_adv), _stream_handle(stream)), "grpo_group_advantages")
+
+
+def sara_gumbel_fast_max_error(stream=None):
+    out = ctypes.c_double(0.0)
+    _check(_lib.sara_gumbel_fast_max_error(ctypes.byref(out), _stream_handle(stream)),
+           "sara_gumbel_fast_max_error")
+    return out.value
 
 
 def sara_sample_logits(d_logits, d_rid, d_pos, seed, step_index, temperature, eos_id, forced_eos_u32,

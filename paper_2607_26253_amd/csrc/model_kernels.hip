@@ -16,6 +16,7 @@
 #include "sara_internal.h"
 
 #include <math.h>
+#include <string.h>
 
 #include <algorithm>
 
@@ -60,6 +61,61 @@ __device__ __forceinline__ int64_t tiled_index(int64_t row, int64_t k, int64_t K
   const int64_t tile = row >> 4, ks = k >> 5, lane = (row & 15) + 16 * ((k >> 3) & 3);
   return ((tile * (K >> 5) + ks) * 64 + lane) * 8 + (k & 7);
 }
+
+// ---------------------------------------------------------------------------
+// Gumbel-max sampling helpers
+// ---------------------------------------------------------------------------
+// score_v = fp32(logit_v / T) + fp32(-log(-log u_v)), u_v = ((w >> 8) + 1/2) 2^-24
+// from word v % 4 of Philox(rid, gen, v / 4, 0); the token is the lowest id
+// of the maximal score.
+__device__ __forceinline__ void better(float& bs, int& bi, float s, int i) {
+  if (s > bs || (s == bs && i < bi)) { bs = s; bi = i; }
+}
+// The noise as the sampler defines it: fp64 logs, rounded to fp32.
+__device__ __forceinline__ float gumbel_exact(uint32_t w) {
+  const double u = ((double)(w >> 8) + 0.5) * 0x1p-24;
+  return (float)(-log(-log(u)));
+}
+// fp32 estimate of gumbel_exact on the hardware log2 (v_log_f32): -ln(u) for
+// u < 1/2 (u exact in fp32), and -log1p(-d) with d = 1 - u (exact in fp32)
+// otherwise, through log1p(x) = ln(1 + x) x / ((1 + x) - 1) (Goldberg), then
+// -ln of the result.  Its distance to gumbel_exact is below kGumbelFastErr
+// for every one of the 2^24 inputs (sara_gumbel_fast_max_error measures it
+// exhaustively).
+constexpr float kGumbelFastErr = 2e-5f;
+__device__ __forceinline__ float ln_hw(float x) { return __builtin_amdgcn_logf(x) * 0.693147180559945309f; }
+__device__ __forceinline__ float gumbel_fast(uint32_t w) {
+  const uint32_t m = w >> 8;
+  float t;
+  if (m < (1u << 23)) {
+    t = -ln_hw(((float)m + 0.5f) * 0x1p-24f);
+  } else {
+    const float dl = (((float)((1u << 24) - m) - 0.5f) * 0x1p-24f);
+    const float y = 1.0f - dl;
+    t = (y == 1.0f) ? dl : ln_hw(y) * (dl * __builtin_amdgcn_rcpf(y - 1.0f));
+  }
+  return -ln_hw(t);
+}
+// fp32(logit / T); UNIT: T = 1, where the division is exact and skipped.
+template <bool UNIT>
+__device__ __forceinline__ float temper(float x, float temp) { return UNIT ? x : __fdiv_rn(x, temp); }
+// Lower bound on every exact score that can still be maximal, given the
+// largest fast score smax: each fast score is within
+// kGumbelFastErr + 2^-22 |score| of its exact value (the noise error plus
+// the two fp32 roundings of the sum), so candidates lie within twice that
+// of smax (with slack for |score| near |smax|).
+__device__ __forceinline__ float gumbel_candidate_floor(float smax) {
+  return smax - 2.0f * kGumbelFastErr - (fabsf(smax) + 1.0f) * 0x1p-20f;
+}
+
+// Operands of the LM-head GEMM's sampling epilogue.
+struct SampleArgs {
+  const RowDesc* rows;       // decode rows (rid, gen, slot)
+  const CtlParams* cp;       // seed, step index, temperature
+  float* logits;             // optional [slots][V] copy of the logits (parity runs), else null
+  float* best;               // [row][gridDim.x] exact best score of the block's vocabulary range
+  int32_t* idx;              // [row][gridDim.x] its token id
+};
 
 // ---------------------------------------------------------------------------
 // embedding gather + first RMSNorm (decode and prefill rows)
@@ -165,6 +221,141 @@ __global__ __launch_bounds__(256) void k_embed_norm(const int32_t* __restrict__ 
 // ---------------------------------------------------------------------------
 // GEMM: out[s][m][n] = sum_{k in split s} X[m][k] * W[n][k]
 // ---------------------------------------------------------------------------
+// Gumbel-max sampling over this block's vocabulary rows, straight from the
+// LM-head accumulators (no logits round trip through memory).  Lane (row,
+// grp) holds, for activation tile t and weight tile nt, the logits of
+// vocabulary ids v = n0 + 16 nt + 4 grp + q (q < 4) of decode row
+// m_base + 16 t + row: exactly the four ids one Philox call keys.
+//  1. fast scores (fp32 noise, gumbel_fast) and their block maximum per row;
+//  2. exact scores (fp64 noise, gumbel_exact) for the candidates at or above
+//     gumbel_candidate_floor(max): the block's exact winner is always among
+//     them, so the result equals an exact evaluation of every id;
+//  3. exact (score, id) maximum per row to sa.best / sa.idx [m][gridDim.x].
+// LDS: the X staging buffer, free after the k loop.
+// Exact score of vocabulary id 4 b + q of decode rollout (rid, gen), given
+// the tempered logit a = fp32(logit / T).  Out of line: it is called for a
+// handful of candidates per row and block, and keeps the fp64 logs out of
+// the unrolled epilogue.
+__device__ __attribute__((noinline)) float exact_score(float a, uint32_t rid, uint32_t gen, uint32_t b, int q,
+                                                       uint32_t k0, uint32_t k1) {
+  const U32x4 w = philox4x32_10(rid, gen, b, 0u, k0, k1);
+  const uint32_t wq = q == 0 ? w.x : q == 1 ? w.y : q == 2 ? w.z : w.w;
+  return __fadd_rn(a, gumbel_exact(wq));
+}
+
+// One round of the sampling epilogue over activation tiles T0 .. T0 + TC - 1
+// (compile-time tile indices, so the accumulators stay in registers).
+template <int NT, int MT, int TC, int T0, bool UNIT>
+__device__ __forceinline__ void sample_round(const f32x4 (&acc)[NT][MT], int M, int m_base, int N, int n0,
+    const SampleArgs& sa, float temp, uint32_t k0, uint32_t k1, uint16_t* __restrict__ xs) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int row = lane & 15, grp = lane >> 4;
+  float* red_max = (float*)xs;                          // [4][TC][16]
+  float* red_s = red_max + 4 * TC * 16;                 // [4][TC][16]
+  int* red_i = (int*)(red_s + 4 * TC * 16);             // [4][TC][16]
+  // (rid, gen, slot) of the decode rows of this round's tiles
+  int s_rid[TC], s_gen[TC], s_slot[TC];
+#pragma unroll
+  for (int tt = 0; tt < TC; ++tt) {
+    const RowDesc r = sa.rows[min(m_base + 16 * (T0 + tt) + row, M - 1)];
+    s_rid[tt] = r.rid; s_gen[tt] = r.gen; s_slot[tt] = r.slot;
+  }
+  __syncthreads();                                      // LDS: the k loop or the previous round is done
+  float f[NT][TC][4];                                   // fast scores
+#pragma unroll
+  for (int tt = 0; tt < TC; ++tt) {
+    float lmax = -INFINITY;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      const int v0 = n0 + 16 * nt + 4 * grp;
+      const U32x4 w = philox4x32_10((uint32_t)s_rid[tt], (uint32_t)s_gen[tt], (uint32_t)(v0 >> 2), 0u, k0, k1);
+      const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        f[nt][tt][q] = (v0 + q < N) ? __fadd_rn(temper<UNIT>(acc[nt][T0 + tt][q], temp), gumbel_fast(wd[q]))
+                                    : -INFINITY;
+        lmax = fmaxf(lmax, f[nt][tt][q]);
+      }
+    }
+    lmax = fmaxf(lmax, __shfl_xor(lmax, 16, 64));
+    lmax = fmaxf(lmax, __shfl_xor(lmax, 32, 64));
+    if (grp == 0) red_max[(wave * TC + tt) * 16 + row] = lmax;
+  }
+  // optional copy of the logits (parity runs)
+  if (sa.logits) {
+#pragma unroll
+    for (int tt = 0; tt < TC; ++tt) {
+      const int m = m_base + 16 * (T0 + tt) + row;
+      if (m >= M) continue;
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int v = n0 + 16 * nt + 4 * grp + q;
+          if (v < N) sa.logits[(size_t)s_slot[tt] * N + v] = acc[nt][T0 + tt][q];
+        }
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int tt = 0; tt < TC; ++tt) {
+    const float* rm = red_max + tt * 16 + row;
+    const float bmax = fmaxf(fmaxf(rm[0], rm[TC * 16]), fmaxf(rm[2 * TC * 16], rm[3 * TC * 16]));
+    const float floor_ = gumbel_candidate_floor(bmax);
+    float bs = -INFINITY;
+    int bi = 0x7FFFFFFF;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (f[nt][tt][q] >= floor_) {
+          const int v0 = n0 + 16 * nt + 4 * grp;
+          better(bs, bi, exact_score(temper<UNIT>(acc[nt][T0 + tt][q], temp), (uint32_t)s_rid[tt],
+                                     (uint32_t)s_gen[tt], (uint32_t)(v0 >> 2), q, k0, k1), v0 + q);
+        }
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      const float s2 = __shfl_xor(bs, o, 64);
+      const int i2 = __shfl_xor(bi, o, 64);
+      better(bs, bi, s2, i2);
+    }
+    if (grp == 0) { red_s[(wave * TC + tt) * 16 + row] = bs; red_i[(wave * TC + tt) * 16 + row] = bi; }
+  }
+  __syncthreads();
+  if (threadIdx.x < TC * 16) {
+    const int tt = threadIdx.x >> 4, r = threadIdx.x & 15, m = m_base + 16 * (T0 + tt) + r;
+    if (m < M) {
+      float bs = -INFINITY;
+      int bi = 0x7FFFFFFF;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) better(bs, bi, red_s[(w * TC + tt) * 16 + r], red_i[(w * TC + tt) * 16 + r]);
+      sa.best[(size_t)m * gridDim.x + blockIdx.x] = bs;
+      sa.idx[(size_t)m * gridDim.x + blockIdx.x] = bi;
+    }
+  }
+}
+
+template <int NT, int MT>
+__device__ __forceinline__ void sample_epilogue(const f32x4 (&acc)[NT][MT], int M, int m_base, int N, int n0,
+    const SampleArgs& sa, uint16_t* __restrict__ xs) {
+  // activation tiles per round: a divisor of MT
+  constexpr int TC = MT % 4 == 0 ? 4 : (MT % 2 == 0 ? 2 : 1);
+  const CtlParams* cp = sa.cp;
+  const float temp = cp->temperature;
+  uint32_t k0, k1;
+  sampler_key(cp->seed, cp->step, k0, k1);
+#define SARA_SR(r, U) \
+  if constexpr (MT > (r) * TC) sample_round<NT, MT, TC, (r) * TC, U>(acc, M, m_base, N, n0, sa, temp, k0, k1, xs);
+  if (temp == 1.0f) {
+    SARA_SR(0, true) SARA_SR(1, true) SARA_SR(2, true) SARA_SR(3, true)
+    SARA_SR(4, true) SARA_SR(5, true) SARA_SR(6, true) SARA_SR(7, true)
+  } else {
+    SARA_SR(0, false) SARA_SR(1, false) SARA_SR(2, false) SARA_SR(3, false)
+    SARA_SR(4, false) SARA_SR(5, false) SARA_SR(6, false) SARA_SR(7, false)
+  }
+#undef SARA_SR
+}
+
 // One m-block of MT 16-row tiles.  Block = 4 waves; wave w owns weight rows
 // [n0, n0 + 16*NT) and all 16*MT activation rows.  The k loop is a 4-slot
 // software pipeline: stage s loads the X chunk (block-cooperative) and the
@@ -178,10 +369,12 @@ __global__ __launch_bounds__(256) void k_embed_norm(const int32_t* __restrict__ 
 // EPI = 1: SwiGLU epilogue (one split only): the weight rows are interleaved
 //          per 16-row tile as gate (even tiles) and up (odd tiles) of the same
 //          16 features; out receives bf16 silu(g) * u as [m][N/2].
+// EPI = 2: Gumbel-max sampling epilogue of the LM head (one split only), see
+//          sample_epilogue; out is unused.
 template <int NT, int MT, int KC, int EPI>
 __device__ __forceinline__ void gemm_mblock(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
     void* __restrict__ out, int M, int m_base, int N, int K, int kps, int64_t split_stride,
-    uint16_t* __restrict__ xs) {
+    uint16_t* __restrict__ xs, const SampleArgs& sa) {
   constexpr int MR = 16 * MT;
   constexpr int PITCH = KC + 8;                 // halves: rows shift by 4 banks, conflict-free b128 reads
   constexpr int C8 = KC / 8;                    // uint4 per X row per chunk
@@ -261,7 +454,9 @@ __device__ __forceinline__ void gemm_mblock(const uint16_t* __restrict__ X, cons
     load(s2, base + 6);
     if (base >= 0) consume(s3, 1, base + 3);
   }
-  if (EPI == 0) {
+  if constexpr (EPI == 2) {
+    sample_epilogue<NT, MT>(acc, M, m_base, N, n0, sa, xs);
+  } else if (EPI == 0) {
     float* o = (float*)out + (size_t)blockIdx.y * split_stride;
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -307,14 +502,14 @@ __device__ __forceinline__ void gemm_mblock(const uint16_t* __restrict__ X, cons
 template <int NT, int MTMAX, int KC, int EPI, int PF>
 __global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __restrict__ X,
     const uint16_t* __restrict__ W, void* __restrict__ out, const int32_t* __restrict__ M_ptr,
-    int N, int K, int kps, int64_t split_stride) {
+    int N, int K, int kps, int64_t split_stride, SampleArgs sa) {
   __shared__ __attribute__((aligned(16))) uint16_t xs[2 * 16 * MTMAX * (KC + 8)];
   const int M = *M_ptr;
   for (int m_base = blockIdx.z * 16 * MTMAX; m_base < M; m_base += gridDim.z * 16 * MTMAX) {
     const int mt = min(MTMAX, (M - m_base + 15) >> 4);
 #define SARA_MB(c) \
     if constexpr (MTMAX >= c) { \
-      if (mt == c) gemm_mblock<NT, c, KC, EPI>(X, W, out, M, m_base, N, K, kps, split_stride, xs); \
+      if (mt == c) gemm_mblock<NT, c, KC, EPI>(X, W, out, M, m_base, N, K, kps, split_stride, xs, sa); \
     }
     SARA_MB(1) SARA_MB(2) SARA_MB(3) SARA_MB(4) SARA_MB(5) SARA_MB(6) SARA_MB(7) SARA_MB(8)
 #undef SARA_MB
@@ -1282,11 +1477,7 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const int32_t* __restrict__
 // ---------------------------------------------------------------------------
 // sampler: Gumbel-max over the vocabulary with Philox4x32-10 noise
 // ---------------------------------------------------------------------------
-// score_v = fp32(logit_v / T) + fp32(-log(-log u_v)), u_v from word v % 4 of
-// Philox(rid, gen, v / 4, 0); the token is the lowest id of the max score.
-__device__ __forceinline__ void better(float& bs, int& bi, float s, int i) {
-  if (s > bs || (s == bs && i < bi)) { bs = s; bi = i; }
-}
+// (score definition and helpers: see "Gumbel-max sampling helpers")
 
 __global__ __launch_bounds__(256) void k_sample_partial(const int32_t* __restrict__ M_ptr,
     const int32_t* __restrict__ rid_arr, const int32_t* __restrict__ pos_arr,
@@ -1317,9 +1508,7 @@ __global__ __launch_bounds__(256) void k_sample_partial(const int32_t* __restric
     for (int e = 0; e < 4; ++e) {
       int v = 4 * b + e;
       if (v < V) {
-        double u = ((double)(ws[e] >> 8) + 0.5) * 0x1p-24;
-        float gmb = (float)(-log(-log(u)));
-        float s = __fadd_rn(__fdiv_rn(lg[v], temp), gmb);
+        float s = __fadd_rn(__fdiv_rn(lg[v], temp), gumbel_exact(ws[e]));
         better(bs, bi, s, v);
       }
     }
@@ -1363,47 +1552,73 @@ __device__ __forceinline__ bool forced_eos_fires(uint64_t seed, int32_t step, in
   return w.x < thr;
 }
 
-// Final token of each decode row: forced EOS, teacher forcing, forced length,
-// reward hash chain, termination and the per-slot finish flag.
+// Final token of each decode row: the best of the row's nchunks partial
+// (score, id) winners, forced EOS, teacher forcing, forced length, reward
+// hash chain, termination and the per-slot finish flag.  One block per row
+// (persistent over the live rows); the (score desc, id asc) order is total,
+// so the reduction order does not matter.
 __global__ __launch_bounds__(256) void k_sample_final(const Ctl* __restrict__ ctl,
     const RowDesc* __restrict__ rows, const float* __restrict__ best,
-    const int32_t* __restrict__ bidx, const int32_t* __restrict__ forced,
+    const int32_t* __restrict__ bidx, int nchunks, const int32_t* __restrict__ forced,
     const int32_t* __restrict__ flen, int model_free, const CtlParams* __restrict__ cpp,
     const double* __restrict__ p, int32_t* __restrict__ out_tok, int32_t* __restrict__ samp_tok,
     int32_t* __restrict__ slot_gen, uint64_t* __restrict__ slot_hash, int32_t* __restrict__ fin,
     int32_t* __restrict__ r_len, int32_t* __restrict__ r_reward) {
-  int M = ctl->done ? 0 : ctl->M;
-  int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= M) return;
-  const CtlParams cp = *cpp;
-  if (!cp.has_flen) flen = nullptr;
-  const RowDesc r = rows[i];
-  const int rid = r.rid, gen = r.gen, s = r.slot;
-  int samp;
-  if (model_free) {
-    samp = forced[(size_t)rid * cp.max_new + gen];
-  } else {
-    samp = reduce_chunks(best, bidx, i);
-    if (cp.eos >= 0 && forced_eos_fires(cp.seed, cp.step, rid, gen, cp.forced_eos)) samp = cp.eos;
-  }
-  int tok = forced ? forced[(size_t)rid * cp.max_new + gen] : samp;
-  bool done = false;
-  if (flen && gen + 1 == flen[rid]) {
-    if (cp.eos >= 0) tok = cp.eos;
-    done = true;
-  }
-  if (cp.eos >= 0 && tok == cp.eos) done = true;
-  if (gen + 1 == cp.max_new) done = true;
-  out_tok[(size_t)rid * cp.max_new + gen] = tok;
-  samp_tok[(size_t)rid * cp.max_new + gen] = samp;
-  uint64_t hsh = mix64(slot_hash[s] ^ (uint64_t)(uint32_t)(tok + 1));
-  slot_hash[s] = hsh;
-  slot_gen[s] = gen + 1;
-  if (done) {
-    r_len[rid] = gen + 1;
-    double u = (double)(hsh >> 11) * 0x1p-53;
-    r_reward[rid] = (u < p[r.uid]) ? 1 : 0;
-    fin[s] = 1;
+  __shared__ float sb[256];
+  __shared__ int si[256];
+  const int M = ctl->done ? 0 : ctl->M;
+  for (int i = blockIdx.x; i < M; i += gridDim.x) {
+    float bs = -INFINITY;
+    int bi = 0x7FFFFFFF;
+    if (!model_free)
+      for (int c = threadIdx.x; c < nchunks; c += 256)
+        better(bs, bi, best[(size_t)i * nchunks + c], bidx[(size_t)i * nchunks + c]);
+    sb[threadIdx.x] = bs;
+    si[threadIdx.x] = bi;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+      if (threadIdx.x < o) {
+        float s2 = sb[threadIdx.x];
+        int i2 = si[threadIdx.x];
+        better(s2, i2, sb[threadIdx.x + o], si[threadIdx.x + o]);
+        sb[threadIdx.x] = s2;
+        si[threadIdx.x] = i2;
+      }
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+      const CtlParams cp = *cpp;
+      const int32_t* fl = cp.has_flen ? flen : nullptr;
+      const RowDesc r = rows[i];
+      const int rid = r.rid, gen = r.gen, s = r.slot;
+      int samp;
+      if (model_free) {
+        samp = forced[(size_t)rid * cp.max_new + gen];
+      } else {
+        samp = si[0];
+        if (cp.eos >= 0 && forced_eos_fires(cp.seed, cp.step, rid, gen, cp.forced_eos)) samp = cp.eos;
+      }
+      int tok = forced ? forced[(size_t)rid * cp.max_new + gen] : samp;
+      bool done = false;
+      if (fl && gen + 1 == fl[rid]) {
+        if (cp.eos >= 0) tok = cp.eos;
+        done = true;
+      }
+      if (cp.eos >= 0 && tok == cp.eos) done = true;
+      if (gen + 1 == cp.max_new) done = true;
+      out_tok[(size_t)rid * cp.max_new + gen] = tok;
+      samp_tok[(size_t)rid * cp.max_new + gen] = samp;
+      uint64_t hsh = mix64(slot_hash[s] ^ (uint64_t)(uint32_t)(tok + 1));
+      slot_hash[s] = hsh;
+      slot_gen[s] = gen + 1;
+      if (done) {
+        r_len[rid] = gen + 1;
+        double u = (double)(hsh >> 11) * 0x1p-53;
+        r_reward[rid] = (u < p[r.uid]) ? 1 : 0;
+        fin[s] = 1;
+      }
+    }
+    __syncthreads();   // sb/si are reused by the next row
   }
 }
 
@@ -1465,7 +1680,7 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     const uint16_t* Wh = (const uint16_t*)W;
 #define SARA_GEMM(NT_, KC_, PF_) \
     hipLaunchKernelGGL((k_gemm_bf16_lds<NT_, MT, KC_, 0, PF_>), grid, dim3(256), 0, c->stream, Xh, Wh, \
-                       (void*)c->ws, M_ptr, N, K, kps, stride)
+                       (void*)c->ws, M_ptr, N, K, kps, stride, SampleArgs{})
     if (c->in_prefill) {
       if (two) SARA_GEMM(2, 64, 1);
       else SARA_GEMM(1, 64, 1);
@@ -1504,10 +1719,10 @@ static void gemm_swiglu(sara_ctx* c, const void* X, const void* W, const int32_t
   dim3 grid((N + 127) / 128, 1, c->in_prefill ? (M_cap + 16 * MT - 1) / (16 * MT) : 1);
   if (c->in_prefill)
     hipLaunchKernelGGL((k_gemm_bf16_lds<2, MT, 64, 1, 1>), grid, dim3(256), 0, c->stream, (const uint16_t*)X,
-                       (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0);
+                       (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0, SampleArgs{});
   else
     hipLaunchKernelGGL((k_gemm_bf16_lds<2, MT, 64, 1, 0>), grid, dim3(256), 0, c->stream, (const uint16_t*)X,
-                       (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0);
+                       (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0, SampleArgs{});
 }
 
 // persistent attention grid: enough blocks for two per CU, never more than items
@@ -1691,29 +1906,43 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
                        c->md.rms_eps, c->h, (float*)c->x, c->U, c->PB, c->SB, c->rope, c->hd / 2,
                        c->row_rope, 0);
   PROF_E(c, kPEmbed, c->d, 0);
+  int nchunks = kSampleChunks;
   if (!model_free) {
-    if (c->md.dtype == SARA_BF16) layers<uint16_t>(c, c->rows_M, S, true);
-    else layers<float>(c, c->rows_M, S, true);
-    int sp;
-    // one K split: ws then holds the logits [M][V] directly
-    PROF_B(c);
-    gemm(c, c->x, c->lm_head, c->rows_M, S, c->V, c->d, sp, 1);
-    PROF_E(c, kPGemmLM, c->V, c->d);
-    PROF_B(c);
-    hipLaunchKernelGGL(k_sample_partial, dim3(std::min(S * kSampleChunks, 2048)), dim3(256), 0, st, c->rows_M,
-                       (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, c->ws, c->V,
-                       (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, c->samp_best, c->samp_idx);
-    PROF_E(c, kPSampleP, c->V, 0);
-    if (logits) {
+    if (c->md.dtype == SARA_BF16) {
+      layers<uint16_t>(c, c->rows_M, S, true);
+      // LM head with the Gumbel-max sampling epilogue: per (row, 128-id block)
+      // exact winners, reduced by k_sample_final
+      const int nb = (c->V + 127) / 128;
+      nchunks = nb;
       PROF_B(c);
-      hipLaunchKernelGGL(k_copy_logits, dim3(64, S), dim3(256), 0, st, c->ctl, c->rows, c->ws, c->V,
-                         logits);
-      PROF_E(c, kPCopy, c->V, 0);
+      hipLaunchKernelGGL((k_gemm_bf16_lds<2, 8, 64, 2, 0>), dim3(nb, 1, 1), dim3(256), 0, st,
+                         (const uint16_t*)c->x, (const uint16_t*)c->lm_head, (void*)nullptr, c->rows_M, c->V,
+                         c->d, c->d, (int64_t)0,
+                         SampleArgs{c->rows, (const CtlParams*)c->cp_dev, logits, c->samp_best, c->samp_idx});
+      PROF_E(c, kPGemmLM, c->V, c->d);
+    } else {
+      layers<float>(c, c->rows_M, S, true);
+      int sp;
+      // one K split: ws then holds the logits [M][V] directly
+      PROF_B(c);
+      gemm(c, c->x, c->lm_head, c->rows_M, S, c->V, c->d, sp, 1);
+      PROF_E(c, kPGemmLM, c->V, c->d);
+      PROF_B(c);
+      hipLaunchKernelGGL(k_sample_partial, dim3(std::min(S * kSampleChunks, 2048)), dim3(256), 0, st,
+                         c->rows_M, (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, c->ws, c->V,
+                         (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, c->samp_best, c->samp_idx);
+      PROF_E(c, kPSampleP, c->V, 0);
+      if (logits) {
+        PROF_B(c);
+        hipLaunchKernelGGL(k_copy_logits, dim3(64, S), dim3(256), 0, st, c->ctl, c->rows, c->ws, c->V,
+                           logits);
+        PROF_E(c, kPCopy, c->V, 0);
+      }
     }
   }
   PROF_B(c);
-  hipLaunchKernelGGL(k_sample_final, dim3((S + 255) / 256), dim3(256), 0, st, c->ctl, c->rows,
-                     c->samp_best, c->samp_idx, forced, c->flen, model_free,
+  hipLaunchKernelGGL(k_sample_final, dim3(std::min(S, 1024)), dim3(256), 0, st, c->ctl, c->rows,
+                     c->samp_best, c->samp_idx, nchunks, forced, c->flen, model_free,
                      (const CtlParams*)c->cp_dev, c->p, c->out_tok, c->samp_tok, c->slot_gen, c->slot_hash, c->fin,
                      c->r_len, c->r_reward);
   PROF_E(c, kPSampleF, 0, 0);
@@ -1745,6 +1974,37 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
   (void)hipFreeAsync(mdev, st);
   e = hipStreamSynchronize(st);
   if (e != hipSuccess) return hip_fail(e, "sample_rows");
+  return SARA_OK;
+}
+
+// Largest |gumbel_fast - gumbel_exact| over all 2^24 noise inputs (the
+// 24-bit mantissa source of u); non-negative floats order like their bits.
+__global__ __launch_bounds__(256) void k_gumbel_check(uint32_t* out) {
+  float e = 0.f;
+  for (uint32_t m = blockIdx.x * 256 + threadIdx.x; m < (1u << 24); m += gridDim.x * 256) {
+    const uint32_t w = m << 8;
+    e = fmaxf(e, fabsf(gumbel_fast(w) - gumbel_exact(w)));
+  }
+  e = wave_max(e);
+  if ((threadIdx.x & 63) == 0) atomicMax(out, __float_as_uint(e));
+}
+
+int launch_gumbel_check(double* h_out, hipStream_t st) {
+  uint32_t* d = nullptr;
+  hipError_t e = hipMallocAsync((void**)&d, sizeof(uint32_t), st);
+  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
+  e = hipMemsetAsync(d, 0, sizeof(uint32_t), st);
+  if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+  hipLaunchKernelGGL(k_gumbel_check, dim3(1024), dim3(256), 0, st, d);
+  uint32_t bits = 0;
+  e = hipMemcpyAsync(&bits, d, sizeof(uint32_t), hipMemcpyDeviceToHost, st);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  (void)hipFreeAsync(d, st);
+  e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return hip_fail(e, "gumbel check");
+  float f;
+  memcpy(&f, &bits, sizeof(f));
+  *h_out = (double)f;
   return SARA_OK;
 }
 

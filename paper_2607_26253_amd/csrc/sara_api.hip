@@ -34,8 +34,8 @@ static int einval(const std::string& msg) {
 }
 
 const char* const kProfNames[kPNumClasses] = {
-    "k_gemm_bf16_lds<1,8,64,0,0>", "k_gemm_bf16_lds<2,8,64,1,0>", "k_gemm_bf16_lds<2,8,64,0,0>",
-    "k_attn_mfma<128>", "k_attn_combine", "k_qkv_epilogue", "k_residual_norm", "k_swiglu",
+    "k_gemm_bf16_lds<1,8,64,0,0>", "k_gemm_bf16_lds<2,8,64,1,0>", "k_gemm_bf16_lds<2,8,64,2,0>",
+    "k_attn_dec<128>", "k_attn_combine", "k_qkv_epilogue", "k_residual_norm_v", "k_swiglu",
     "k_embed_norm", "k_sample_partial", "k_sample_final", "k_decode_rows", "k_copy_logits", "k_qkv_rope",
     ".gemm[q|k|v]", ".gemm[o]", ".gemm[gate|up]", ".gemm[down]", ".gemm[lm_head]"};
 
@@ -289,8 +289,11 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
                           (size_t)std::max((int64_t)c->row_cap * c->attn_splits_max,
                                            (int64_t)c->S * c->dec_splits_max) *
                           c->hkv * kMaxGroup * (c->hd + 2));
-  ALLOC(c->samp_best, sizeof(float) * (size_t)c->S * kSampleChunks);
-  ALLOC(c->samp_idx, sizeof(int32_t) * (size_t)c->S * kSampleChunks);
+  // per (row, vocabulary chunk) winners: kSampleChunks chunks (fp32 models),
+  // one per 128-id block of the fused LM-head sampler (bf16 models)
+  const size_t nchunk = std::max<size_t>(kSampleChunks, (size_t)(c->V + 127) / 128);
+  ALLOC(c->samp_best, sizeof(float) * (size_t)c->S * nchunk);
+  ALLOC(c->samp_idx, sizeof(int32_t) * (size_t)c->S * nchunk);
   ALLOC(c->g_off, sizeof(int32_t) * (c->U + 1));
   ALLOC(c->g_r, sizeof(float) * nroll);
   ALLOC(c->g_adv, sizeof(float) * nroll);
@@ -673,6 +676,11 @@ extern "C" int sara_sample_logits(const float* d_logits, int32_t n_rows, int32_t
   if (eos_id >= vocab) return einval("eos_id out of range");
   return launch_sample_rows(d_logits, n_rows, vocab, d_rid, d_pos, seed, step_index, temperature, eos_id,
                             forced_eos_u32, d_tok, (hipStream_t)stream);
+}
+
+extern "C" int sara_gumbel_fast_max_error(double* h_out, void* stream) {
+  if (!h_out) return einval("h_out is null");
+  return launch_gumbel_check(h_out, (hipStream_t)stream);
 }
 
 extern "C" void sara_destroy(sara_ctx* c) {

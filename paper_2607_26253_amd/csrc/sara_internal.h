@@ -197,6 +197,7 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
                        const int32_t* pos, uint64_t seed, int step, float temp, int eos,
                        uint32_t feos, int32_t* tok, hipStream_t st);
 int launch_convert_norms(sara_ctx* c, const void* const* w);
+int launch_gumbel_check(double* h_out, hipStream_t st);
 int launch_tile_weights(sara_ctx* c, const void* src, void* dst, int rows, int K, int tile_mul, int tile_add);
 int launch_tile_weights_pairs(sara_ctx* c, const void* src, void* dst, int n_rows, int K, int head_off);
 
@@ -229,8 +230,10 @@ __device__ __forceinline__ U32x4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     if (r > 0) { k0 += 0x9E3779B9u; k1 += 0xBB67AE85u; }
-    uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
-    uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+    // full 64-bit products: one multiply instruction per product on gfx950
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0, p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t lo0 = (uint32_t)p0, hi0 = (uint32_t)(p0 >> 32);
+    const uint32_t lo1 = (uint32_t)p1, hi1 = (uint32_t)(p1 >> 32);
     uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
     c0 = n0; c1 = lo1; c2 = n2; c3 = lo0;
   }

@@ -82,6 +82,29 @@ def check_sampler_on_oracle_logits(cfg, ora, seed, step):
     assert ties <= 1
 
 
+def check_fused_sampler_exact(cfg, gpu, seed, step):
+    """The LM head's fused sampler (fast noise, exact re-scoring of the
+    candidates) must pick exactly what the exact sampler picks on the same
+    GPU logits: every sampled token, no tie allowance."""
+    import torch
+
+    import paper_2607_26253_amd as sara
+    k = cfg["alloc"]["k"]
+    rows = sorted(slot_rows(gpu).items())
+    lg = np.stack([gpu["logits"][t][s] for (t, s), _ in rows]).astype(np.float32)
+    rid = np.array([u * k + j for _, (u, j, i) in rows], np.int32)
+    pos = np.array([i for _, (u, j, i) in rows], np.int32)
+    d_tok = torch.empty(len(rows), dtype=torch.int32, device="cuda")
+    a, m = cfg["alloc"], cfg["model"]
+    sara.sara_sample_logits(torch.from_numpy(lg).cuda(), torch.from_numpy(rid).cuda(),
+                            torch.from_numpy(pos).cuda(), seed, step, a["temperature"],
+                            m["eos_id"], a["forced_eos_u32"], d_tok)
+    want = d_tok.cpu().numpy()
+    got = np.array([gpu["roll"]["sampled"][u * k + j][i] for _, (u, j, i) in rows])
+    assert np.array_equal(got, want), np.nonzero(got != want)
+    return len(rows)
+
+
 @pytest.mark.parametrize("name", list(SLICES))
 def test_bf16_slice_full_depth(name):
     import torch
@@ -110,6 +133,8 @@ def test_bf16_slice_full_depth(name):
     assert worst_rms <= 3e-2
     assert worst_max <= max(3e-2, 2.0 * floor)
     check_sampler_on_oracle_logits(cfg, ora, seed, pool["step"])
+    n = check_fused_sampler_exact(cfg, gpu, seed, pool["step"])
+    print(f"[slice] fused LM-head sampler = exact sampler on {n} GPU logit rows", flush=True)
     k = cfg["alloc"]["k"]
     agree, total = 0, 0
     for (u, j), d in ora["rollouts_detail"].items():
@@ -135,4 +160,5 @@ def test_bf16_two_layer_truncation_strict(name):
     worst_max = max(e["max"] for e in errs)
     print(f"[slice-2L] {name}: max|d|/rms {worst_max:.4f}", flush=True)
     assert worst_max <= 3e-2
+    check_fused_sampler_exact(cfg, gpu, seed, pool["step"])
     ctx.close()
