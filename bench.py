@@ -76,7 +76,7 @@ def cpu_baseline(cfg, weights, seconds_target=15.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="qwen1p5b_shape")
     ap.add_argument("--graph-iters", type=int, default=16)
@@ -115,8 +115,11 @@ def main():
         d_fl = torch.from_numpy(np.ascontiguousarray(p["forced_len"].reshape(-1))).cuda() \
             if p["forced_len"] is not None else None
         ctx.sara_begin_step(d_tok, p["offsets"], d_p, d_fl, p["step"])
+        torch.cuda.synchronize()
+        print("[bench] decode-iters: prefill done", file=sys.stderr, flush=True)
         ctx.sara_run(None, graph_iters=args.graph_iters, max_iters=args.graph_iters)
         torch.cuda.synchronize()
+        print("[bench] decode-iters: graph captured and replayed once", file=sys.stderr, flush=True)
         t0 = time.perf_counter()
         n = ctx.sara_run(None, graph_iters=args.graph_iters, max_iters=args.decode_iters)
         dt = time.perf_counter() - t0

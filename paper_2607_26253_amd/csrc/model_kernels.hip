@@ -113,8 +113,9 @@ struct SampleArgs {
   const RowDesc* rows;       // decode rows (rid, gen, slot)
   const CtlParams* cp;       // seed, step index, temperature
   float* logits;             // optional [slots][V] copy of the logits (parity runs), else null
-  float* best;               // [row][gridDim.x] exact best score of the block's vocabulary range
-  int32_t* idx;              // [row][gridDim.x] its token id
+  float* best;               // [gridDim.x][ld] exact best score of the block's vocabulary range per row
+  int32_t* idx;              // [gridDim.x][ld] its token id
+  int ld;                    // row stride of best / idx (>= the live row count)
 };
 
 // ---------------------------------------------------------------------------
@@ -329,8 +330,8 @@ __device__ __forceinline__ void sample_round(const f32x4 (&acc)[NT][MT], int M, 
       int bi = 0x7FFFFFFF;
 #pragma unroll
       for (int w = 0; w < 4; ++w) better(bs, bi, red_s[(w * TC + tt) * 16 + r], red_i[(w * TC + tt) * 16 + r]);
-      sa.best[(size_t)m * gridDim.x + blockIdx.x] = bs;
-      sa.idx[(size_t)m * gridDim.x + blockIdx.x] = bi;
+      sa.best[(size_t)blockIdx.x * sa.ld + m] = bs;
+      sa.idx[(size_t)blockIdx.x * sa.ld + m] = bi;
     }
   }
 }
@@ -1553,13 +1554,14 @@ __device__ __forceinline__ bool forced_eos_fires(uint64_t seed, int32_t step, in
 }
 
 // Final token of each decode row: the best of the row's nchunks partial
-// (score, id) winners, forced EOS, teacher forcing, forced length, reward
+// (score, id) winners (chunk c of row i at [c * cstride + i * rstride]),
+// forced EOS, teacher forcing, forced length, reward
 // hash chain, termination and the per-slot finish flag.  One block per row
 // (persistent over the live rows); the (score desc, id asc) order is total,
 // so the reduction order does not matter.
 __global__ __launch_bounds__(256) void k_sample_final(const Ctl* __restrict__ ctl,
     const RowDesc* __restrict__ rows, const float* __restrict__ best,
-    const int32_t* __restrict__ bidx, int nchunks, const int32_t* __restrict__ forced,
+    const int32_t* __restrict__ bidx, int nchunks, int cstride, int rstride, const int32_t* __restrict__ forced,
     const int32_t* __restrict__ flen, int model_free, const CtlParams* __restrict__ cpp,
     const double* __restrict__ p, int32_t* __restrict__ out_tok, int32_t* __restrict__ samp_tok,
     int32_t* __restrict__ slot_gen, uint64_t* __restrict__ slot_hash, int32_t* __restrict__ fin,
@@ -1572,7 +1574,7 @@ __global__ __launch_bounds__(256) void k_sample_final(const Ctl* __restrict__ ct
     int bi = 0x7FFFFFFF;
     if (!model_free)
       for (int c = threadIdx.x; c < nchunks; c += 256)
-        better(bs, bi, best[(size_t)i * nchunks + c], bidx[(size_t)i * nchunks + c]);
+        better(bs, bi, best[(size_t)c * cstride + (size_t)i * rstride], bidx[(size_t)c * cstride + (size_t)i * rstride]);
     sb[threadIdx.x] = bs;
     si[threadIdx.x] = bi;
     __syncthreads();
@@ -1918,7 +1920,7 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
       hipLaunchKernelGGL((k_gemm_bf16_lds<2, 8, 64, 2, 0>), dim3(nb, 1, 1), dim3(256), 0, st,
                          (const uint16_t*)c->x, (const uint16_t*)c->lm_head, (void*)nullptr, c->rows_M, c->V,
                          c->d, c->d, (int64_t)0,
-                         SampleArgs{c->rows, (const CtlParams*)c->cp_dev, logits, c->samp_best, c->samp_idx});
+                         SampleArgs{c->rows, (const CtlParams*)c->cp_dev, logits, c->samp_best, c->samp_idx, S});
       PROF_E(c, kPGemmLM, c->V, c->d);
     } else {
       layers<float>(c, c->rows_M, S, true);
@@ -1941,8 +1943,11 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
     }
   }
   PROF_B(c);
+  // chunk winners: [row][kSampleChunks] from k_sample_partial, [chunk][S] from the fused LM head
+  const bool fused = !model_free && c->md.dtype == SARA_BF16;
   hipLaunchKernelGGL(k_sample_final, dim3(std::min(S, 1024)), dim3(256), 0, st, c->ctl, c->rows,
-                     c->samp_best, c->samp_idx, nchunks, forced, c->flen, model_free,
+                     c->samp_best, c->samp_idx, nchunks, fused ? S : 1, fused ? 1 : nchunks, forced, c->flen,
+                     model_free,
                      (const CtlParams*)c->cp_dev, c->p, c->out_tok, c->samp_tok, c->slot_gen, c->slot_hash, c->fin,
                      c->r_len, c->r_reward);
   PROF_E(c, kPSampleF, 0, 0);

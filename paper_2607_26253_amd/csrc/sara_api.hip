@@ -72,8 +72,12 @@ int prof_collect(sara_ctx* c) {
     HIP_TRY(hipEventElapsedTime(&ms, c->prof_events[r.e0], c->prof_events[r.e1]), "elapsed");
     double by = 0.0, fl = 0.0, N = r.N, K = r.K;
     switch (r.cls) {
-      case kPGemmN1: case kPGemmLM:
+      case kPGemmN1:
         by = N * K * E + m * K * E + m * N * 4.0; fl = 2.0 * m * N * K; break;
+      case kPGemmLM:   // bf16: sampling epilogue, one (score, id) per row and 128-id block
+        by = N * K * E + m * K * E + (E == 2 ? m * ((N + 127) / 128) * 8.0 : m * N * 4.0);
+        fl = 2.0 * m * N * K;
+        break;
       case kPGemmGU:   // output is the bf16 SwiGLU product [m][N/2]
         by = N * K * E + m * K * E + m * (N / 2) * E; fl = 2.0 * m * N * K; break;
       case kPAttn:
