@@ -84,6 +84,10 @@ def main():
     ap.add_argument("--profile-every", type=int, default=16)
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--counter-pass", type=int, default=0,
+                    help="counter mode: run this many eager decode/decide/refill iterations of step 0 with "
+                         "per-kernel event profiling and print each kernel class's algorithmic bytes per "
+                         "launch (pair it with rocprofv3 --pmc over the same run), then exit")
     ap.add_argument("--decode-iters", type=int, default=0,
                     help="profiling mode: only replay this many decode/decide/refill iterations of "
                          "step 0 from the HIP graph (for kernel traces), then exit")
@@ -108,6 +112,31 @@ def main():
     del dw
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+    if args.counter_pass:
+        p = W.make_pool(cfg, 0)
+        d_tok, d_p = torch.from_numpy(p["tokens"]).cuda(), torch.from_numpy(p["p"]).cuda()
+        d_fl = torch.from_numpy(np.ascontiguousarray(p["forced_len"].reshape(-1))).cuda() \
+            if p["forced_len"] is not None else None
+        ctx.sara_begin_step(d_tok, p["offsets"], d_p, d_fl, p["step"])
+        torch.cuda.synchronize()
+        print("[bench] counter pass: prefill done", file=sys.stderr, flush=True)
+        ctx.sara_reset_profile()
+        ctx.sara_set_profiling(True)
+        for it in range(args.counter_pass):
+            ctx.sara_decode_step(None, None, False)
+            ctx.sara_posterior_decide()
+            ctx.sara_refill()
+        ctx.sara_set_profiling(False)
+        prof = ctx.sara_read_profile()
+        q = ctx.sara_query()
+        print(json.dumps({"mode": "counter_pass", "workload": describe(cfg), "iters": args.counter_pass,
+                          "running_slots": q["running"],
+                          "classes": {k["name"]: {"launches": k["launches"],
+                                                  "alg_bytes_per_launch": k["bytes"] / k["launches"]}
+                                      for k in prof if k["launches"] > 0}}), flush=True)
+        ctx.close()
+        return
 
     if args.decode_iters:
         p = W.make_pool(cfg, 0)

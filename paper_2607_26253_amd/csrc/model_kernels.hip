@@ -614,18 +614,6 @@ __device__ __forceinline__ float split_sum(const float* ws, int splits, int64_t 
 // serialise the memory round trips.
 __device__ __forceinline__ float mask01(bool keep) { return keep ? 1.0f : 0.0f; }
 
-// split_sum for at most kMaxSplitsDec splits with every load in flight at once.
-__device__ __forceinline__ float split_sum8(const float* ws, int splits, int64_t stride, size_t idx) {
-  float v[kMaxSplitsDec];
-#pragma unroll
-  for (int s = 0; s < kMaxSplitsDec; ++s)
-    v[s] = ws[(size_t)min(s, splits - 1) * stride + idx] * mask01(s < splits);
-  float a[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int s = 0; s < kMaxSplitsDec; ++s) a[s & 3] += v[s];
-  return (a[0] + a[1]) + (a[2] + a[3]);
-}
-
 // Page of position pos: block-table entries [0, PB) map the shared prompt
 // segment (positions < plen), entries [PB, MAXB) the private segment that
 // starts at position plen.
@@ -735,7 +723,7 @@ __global__ __launch_bounds__(256) void k_residual_norm_v(const int32_t* __restri
   for (int i = blockIdx.x; i < M; i += gridDim.x) {
     const size_t rb = (size_t)i * d;
     float a0[VPT], a1[VPT], a2[VPT], a3[VPT], hv[VPT];
-    // unconditional loads from clamped indices, masked (see split_sum8)
+    // unconditional loads from clamped indices, masked (see mask01)
     float wv[VPT];
 #pragma unroll
     for (int v = 0; v < VPT; ++v) {
@@ -1448,7 +1436,7 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const int32_t* __restrict__
       float mk[8];
 #pragma unroll
       for (int q = 0; q < 8; ++q) {
-        // unconditional loads from a clamped split index (see split_sum8): the
+        // unconditional loads from a clamped split index (see mask01): the
         // surplus entries repeat split ns - 1 of this chunk, which leaves the
         // maximum unchanged, and their weight is masked to zero
         const float* p = base + (size_t)min(c0 + q, ns - 1) * sstride;
@@ -1670,8 +1658,16 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     const int KC = 64;
     int chunks = K / KC;
     int splits = std::min(want, std::max(1, chunks / 4));
-    // decode consumers sum at most kMaxSplitsDec partials in one batch of loads
-    if (!c->in_prefill) splits = std::min(splits, kMaxSplitsDec);
+    if (!c->in_prefill) {
+      // decode: an even division of the k chunks keeps the splits balanced
+      // (the last split of an uneven one runs alone); take the largest even
+      // count in [6, kMaxSplitsDec] with >= 4 chunks per split, else the
+      // occupancy target.  Consumers sum at most kMaxSplitsDec partials in
+      // one batch of loads.
+      for (int s = kMaxSplitsDec; s >= 6; --s)
+        if (s <= want && chunks % s == 0 && chunks / s >= 4) { splits = s; break; }
+      splits = std::min(splits, kMaxSplitsDec);
+    }
     if (splits > max_splits) splits = max_splits;
     if (splits < 1) splits = 1;
     int kps = ((chunks + splits - 1) / splits) * KC;

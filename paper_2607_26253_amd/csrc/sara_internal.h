@@ -19,7 +19,7 @@ constexpr int kAttnSplit = 256;      // tokens per context split (fp32 VALU atte
 constexpr int kAttnChunks = 16;      // KV pages per context split (bf16 MFMA prefill attention)
 constexpr int kDecPpw = 2;           // KV pages per wave in the decode attention
 constexpr int kDecPages = 4 * kDecPpw;  // KV pages per context split in the decode attention
-constexpr int kMaxSplitsDec = 8;     // split-K partials of a decode GEMM (summed in one batch)
+constexpr int kMaxSplitsDec = 12;    // split-K partials of a decode GEMM (summed in one batch; a multiple of 4)
 constexpr int kAttnTile = 64;        // tokens per LDS tile inside a split
 constexpr int kSampleChunks = 16;    // vocabulary chunks per sampled row
 constexpr int kCtlThreads = 1024;    // threads of the single-workgroup controller
