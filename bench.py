@@ -29,6 +29,30 @@ import workloads as W  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_decode_qwen1p5b_shape_128rows.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_26253_amd", "csrc", "model_kernels.hip")
+
+
+def measured_traffic(kernel):
+    """HBM-side bytes per launch of `kernel` from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary (calibrated on a copy of known size), with
+    the algorithmic bytes of the same launches; None when the summary does not
+    cover the kernel or the kernel source changed since it was taken."""
+    import hashlib
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+        src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    if f"model_kernels.hip sha256 {src}" not in text:
+        return None
+    for line in text.splitlines():
+        cells = [c.strip() for c in line.strip().strip("|").split("|")]
+        if len(cells) == 7 and cells[0] == f"`{kernel}`" and cells[5] != "-":
+            return {"traffic": float(cells[4]), "alg_bytes_per_launch": float(cells[5]), "ratio": float(cells[6]),
+                    "regime": "16 eager decode iterations at 128 rows (first allocation step)",
+                    "source": os.path.relpath(TRAFFIC_PROFILE, ROOT)}
+    return None
 
 
 def describe(cfg):
@@ -247,9 +271,12 @@ def main():
         per_launch_ms = dom["ms"] / dom["launches"]
         per_launch_by = dom["bytes"] / dom["launches"]
         ach = per_launch_by / (per_launch_ms * 1e-3) / 1e9
+        tr = measured_traffic(dom["name"])
         out["roofline"] = {
             "kernel": dom["name"], "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": ach / HBM_PEAK_GBS, "traffic": None,
+            "frac": ach / HBM_PEAK_GBS, "traffic": tr["traffic"] if tr else None,
+            "traffic_measured_at": ({k: tr[k] for k in ("regime", "alg_bytes_per_launch", "ratio", "source")}
+                                    if tr else None),
             "avg_launch_us": per_launch_ms * 1e3, "alg_bytes_per_launch": per_launch_by,
             "launches_timed": dom["launches"],
             "tflops": dom["flops"] / (dom["ms"] * 1e-3) / 1e12 if dom["flops"] else None,

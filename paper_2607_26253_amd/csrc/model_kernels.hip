@@ -15,6 +15,8 @@
 // so results do not depend on scheduling.  The fp32 model uses a VALU GEMM.
 #include "sara_internal.h"
 
+#include <hip/hip_ext.h>
+
 #include <math.h>
 #include <string.h>
 
@@ -1638,6 +1640,21 @@ __global__ void k_copy_logits(const Ctl* __restrict__ ctl, const RowDesc* __rest
 // ---------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------
+// Kernel launch on a context's stream.  While a per-kernel profile record is
+// open (prof_begin), the launch goes through hipExtLaunchKernelGGL with the
+// record's event pair, so the dispatch itself stamps the kernel's start and
+// end: the elapsed time is the kernel's own duration, as in a kernel trace.
+template <typename F, typename... Args>
+static void launch_k(sara_ctx* c, hipStream_t st, F kernel, dim3 grid, dim3 block, uint32_t shm, Args... args) {
+  const int p = c->prof_pending;
+  if (p >= 0) {
+    c->prof_pending = -1;
+    c->prof_last = p;
+    hipExtLaunchKernelGGL(kernel, grid, block, shm, st, c->prof_events[p], c->prof_events[p + 1], 0u, args...);
+  } else {
+    hipLaunchKernelGGL(kernel, grid, block, shm, st, args...);
+  }
+}
 static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr, int M_cap,
                 int N, int K, int& splits_out, int max_splits = 1 << 30) {
   int64_t stride = (int64_t)M_cap * N;
@@ -1677,7 +1694,7 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     const uint16_t* Xh = (const uint16_t*)X;
     const uint16_t* Wh = (const uint16_t*)W;
 #define SARA_GEMM(NT_, KC_, PF_) \
-    hipLaunchKernelGGL((k_gemm_bf16_lds<NT_, MT, KC_, 0, PF_>), grid, dim3(256), 0, c->stream, Xh, Wh, \
+    launch_k(c, c->stream, (k_gemm_bf16_lds<NT_, MT, KC_, 0, PF_>), grid, dim3(256), 0, Xh, Wh, \
                        (void*)c->ws, M_ptr, N, K, kps, stride, SampleArgs{})
     if (c->in_prefill) {
       if (two) SARA_GEMM(2, 64, 1);
@@ -1699,7 +1716,7 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     splits = (K + kps - 1) / kps;
     if ((int64_t)splits * stride > c->ws_floats) { splits = 1; kps = K; }
     dim3 grid(tiles_n, splits, zb);
-    hipLaunchKernelGGL(k_gemm_f32, grid, dim3(256), 0, c->stream, (const float*)X, (const float*)W,
+    launch_k(c, c->stream, k_gemm_f32, grid, dim3(256), 0, (const float*)X, (const float*)W,
                        c->ws, M_ptr, N, K, kps, stride);
     splits_out = splits;
   }
@@ -1716,10 +1733,10 @@ static void gemm_swiglu(sara_ctx* c, const void* X, const void* W, const int32_t
   const int N = 2 * c->ffn, K = c->d;
   dim3 grid((N + 127) / 128, 1, c->in_prefill ? (M_cap + 16 * MT - 1) / (16 * MT) : 1);
   if (c->in_prefill)
-    hipLaunchKernelGGL((k_gemm_bf16_lds<2, MT, 64, 1, 1>), grid, dim3(256), 0, c->stream, (const uint16_t*)X,
+    launch_k(c, c->stream, (k_gemm_bf16_lds<2, MT, 64, 1, 1>), grid, dim3(256), 0, (const uint16_t*)X,
                        (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0, SampleArgs{});
   else
-    hipLaunchKernelGGL((k_gemm_bf16_lds<2, MT, 64, 1, 0>), grid, dim3(256), 0, c->stream, (const uint16_t*)X,
+    launch_k(c, c->stream, (k_gemm_bf16_lds<2, MT, 64, 1, 0>), grid, dim3(256), 0, (const uint16_t*)X,
                        (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0, SampleArgs{});
 }
 
@@ -1736,7 +1753,7 @@ static void residual_norm(sara_ctx* c, const int32_t* M_ptr, int M_cap, int sp, 
   const dim3 grid(std::min(M_cap, 1024));
   const int64_t stride = (int64_t)M_cap * d;
   T* x = (T*)c->x;
-#define SARA_RN(V) hipLaunchKernelGGL((k_residual_norm_v<T, V>), grid, dim3(256), 0, c->stream, M_ptr, c->ws, \
+#define SARA_RN(V) launch_k(c, c->stream, (k_residual_norm_v<T, V>), grid, dim3(256), 0, M_ptr, c->ws, \
                                       sp, stride, d, c->h, w, c->md.rms_eps, x, x_tiled)
   switch (sp <= kMaxSplitsDec ? vpt : 0) {
     case 1: SARA_RN(1); break;
@@ -1746,7 +1763,7 @@ static void residual_norm(sara_ctx* c, const int32_t* M_ptr, int M_cap, int sp, 
     case 5: case 6: SARA_RN(6); break;
     case 7: case 8: SARA_RN(8); break;
     default:
-      hipLaunchKernelGGL(k_residual_norm<T>, dim3(std::min(M_cap, 256)), dim3(1024), 0, c->stream, M_ptr,
+      launch_k(c, c->stream, k_residual_norm<T>, dim3(std::min(M_cap, 256)), dim3(1024), 0, M_ptr,
                          c->ws, sp, stride, d, c->h, w, c->md.rms_eps, x, x_tiled);
   }
 #undef SARA_RN
@@ -1766,7 +1783,7 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
       // paged attention, then the merge of rows with several context splits
       PROF_B(c);
 #define SARA_QKV(KS_) \
-      hipLaunchKernelGGL((k_qkv_rope<HD, KS_>), dim3(c->nqkv / 16), dim3(256), 0, st, (const uint16_t*)x, \
+      launch_k(c, st, (k_qkv_rope<HD, KS_>), dim3(c->nqkv / 16), dim3(256), 0, (const uint16_t*)x, \
                          (const uint16_t*)c->w_qkv[l], M_ptr, d, c->rows, c->row_rope, c->hq, c->hkv, l, \
                          c->n_blocks, (uint16_t*)c->qbuf, (uint16_t*)c->kc, (uint16_t*)c->vc)
       switch (d / 128) {
@@ -1781,12 +1798,12 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
       PROF_E(c, kPQkvRope, c->nqkv, d);
       PROF_B(c);
       const int dg = (int)std::min<int64_t>((int64_t)M_cap * c->hkv * c->dec_splits_max, 2048);
-      hipLaunchKernelGGL((k_attn_dec<HD>), dim3(dg), dim3(256), 0, st, M_ptr, c->rows, (const uint16_t*)c->kc,
+      launch_k(c, st, (k_attn_dec<HD>), dim3(dg), dim3(256), 0, M_ptr, c->rows, (const uint16_t*)c->kc,
                          (const uint16_t*)c->vc, l, c->n_blocks, c->hq, c->hkv, c->dec_splits_max,
                          1.0f / sqrtf((float)HD), (const uint16_t*)c->qbuf, c->attn_part, (uint16_t*)x);
       PROF_E(c, kPAttn, 0, 0);
       PROF_B(c);
-      hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(1024), dim3(HD), 0, st, M_ptr, c->rows,
+      launch_k(c, st, (k_attn_combine<T, HD>), dim3(1024), dim3(HD), 0, M_ptr, c->rows,
                          c->attn_part, c->hq, c->hkv, c->dec_splits_max, kDecPages, 1, x);
       PROF_E(c, kPCombine, 0, 0);
     } else {
@@ -1794,25 +1811,25 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     gemm(c, x, c->w_qkv[l], M_ptr, M_cap, c->nqkv, d, sp);
     PROF_E(c, kPGemmN1, c->nqkv, d);
     PROF_B(c);
-    hipLaunchKernelGGL(k_qkv_epilogue<T>, dim3(2048), dim3(c->hd / 2), 0, st, M_ptr,
+    launch_k(c, st, k_qkv_epilogue<T>, dim3(2048), dim3(c->hd / 2), 0, M_ptr,
                        c->rows, c->ws, sp,
                        stride_qkv, c->rope, c->hq, c->hkv, c->hd, l, c->n_blocks, c->btab, c->MAXB,
                        c->PB, (T*)c->qbuf, (T*)c->kc, (T*)c->vc, mfma_attn ? 1 : 0);
     PROF_E(c, kPQkv, c->nqkv, 0);
     PROF_B(c);
     if (mfma_attn)
-      hipLaunchKernelGGL((k_attn_mfma<HD>), dim3(attn_grid(c, M_cap)), dim3(256), 0, st,
+      launch_k(c, st, (k_attn_mfma<HD>), dim3(attn_grid(c, M_cap)), dim3(256), 0,
                          M_ptr, c->rows, (const uint16_t*)c->qbuf, (const uint16_t*)c->kc,
                          (const uint16_t*)c->vc, c->btab, c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv,
                          c->attn_splits_max, 1.0f / sqrtf((float)HD), c->attn_part);
     else
-      hipLaunchKernelGGL((k_attention<T, HD>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0, st,
+      launch_k(c, st, (k_attention<T, HD>), dim3(M_cap, c->hkv, c->attn_splits_max), dim3(256), 0,
                          M_ptr, c->rows, (const T*)c->qbuf, (const T*)c->kc, (const T*)c->vc, c->btab,
                          c->MAXB, c->PB, l, c->n_blocks, c->hq, c->hkv, c->attn_splits_max,
                          1.0f / sqrtf((float)HD), c->attn_part);
     PROF_E(c, kPAttn, 0, 0);
     PROF_B(c);
-    hipLaunchKernelGGL((k_attn_combine<T, HD>), dim3(1024), dim3(HD), 0, st, M_ptr, c->rows,
+    launch_k(c, st, (k_attn_combine<T, HD>), dim3(1024), dim3(HD), 0, M_ptr, c->rows,
                        c->attn_part, c->hq, c->hkv, c->attn_splits_max, mfma_attn ? kAttnChunks : 0, 0, x);
     PROF_E(c, kPCombine, 0, 0);
     }
@@ -1834,7 +1851,7 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
       gemm(c, x, c->w_gu[l], M_ptr, M_cap, 2 * c->ffn, d, sp);
       PROF_E(c, kPGemmN1, 2 * c->ffn, d);
       PROF_B(c);
-      hipLaunchKernelGGL(k_swiglu<T>, dim3(1024), dim3(256), 0, st, M_ptr, c->ws,
+      launch_k(c, st, k_swiglu<T>, dim3(1024), dim3(256), 0, M_ptr, c->ws,
                          sp, (int64_t)M_cap * 2 * c->ffn, c->ffn, x);
       PROF_E(c, kPSwiglu, c->ffn, 0);
       PROF_B(c);
@@ -1869,15 +1886,15 @@ int launch_prefill(sara_ctx* c) {
   int64_t rows_total = pre[c->U];
   for (int64_t r0 = 0; r0 < rows_total; r0 += c->prefill_rows) {
     int n = (int)((rows_total - r0 < c->prefill_rows) ? rows_total - r0 : c->prefill_rows);
-    hipLaunchKernelGGL(k_prefill_rows, dim3((n + 255) / 256), dim3(256), 0, st, c->pre, c->U, (int)r0,
+    launch_k(c, st, k_prefill_rows, dim3((n + 255) / 256), dim3(256), 0, c->pre, c->U, (int)r0,
                        n, c->tok, c->off, c->S, c->rows, c->rows_M, c->PB);
     if (c->md.dtype == SARA_BF16) {
-      hipLaunchKernelGGL(k_embed_norm<uint16_t>, dim3(n), dim3(256), 0, st, c->rows_M, c->rows,
+      launch_k(c, st, k_embed_norm<uint16_t>, dim3(n), dim3(256), 0, c->rows_M, c->rows,
                          (const uint16_t*)c->embed, c->norms, c->d, c->md.rms_eps, c->h,
                          (uint16_t*)c->x);
       layers<uint16_t>(c, c->rows_M, n, false);
     } else {
-      hipLaunchKernelGGL(k_embed_norm<float>, dim3(n), dim3(256), 0, st, c->rows_M, c->rows,
+      launch_k(c, st, k_embed_norm<float>, dim3(n), dim3(256), 0, c->rows_M, c->rows,
                          (const float*)c->embed, c->norms, c->d, c->md.rms_eps, c->h, (float*)c->x);
       layers<float>(c, c->rows_M, n, false);
     }
@@ -1892,13 +1909,13 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
   PROF_B(c);
   const int eg = std::min(S, 512);
   if (c->md.dtype == SARA_BF16)
-    hipLaunchKernelGGL(k_decode_embed<uint16_t>, dim3(eg), dim3(256), 0, st, c->ctl, c->active, c->slot_uid,
+    launch_k(c, st, k_decode_embed<uint16_t>, dim3(eg), dim3(256), 0, c->ctl, c->active, c->slot_uid,
                        c->slot_j, c->slot_gen, c->tok, c->off, c->out_tok, c->k, c->ad.max_new, c->rows,
                        c->rows_M, model_free ? 0 : 1, (const uint16_t*)c->embed, c->norms, c->d,
                        c->md.rms_eps, c->h, (uint16_t*)c->x, c->U, c->PB, c->SB, c->rope, c->hd / 2,
                        c->row_rope, 1);
   else
-    hipLaunchKernelGGL(k_decode_embed<float>, dim3(eg), dim3(256), 0, st, c->ctl, c->active, c->slot_uid,
+    launch_k(c, st, k_decode_embed<float>, dim3(eg), dim3(256), 0, c->ctl, c->active, c->slot_uid,
                        c->slot_j, c->slot_gen, c->tok, c->off, c->out_tok, c->k, c->ad.max_new, c->rows,
                        c->rows_M, model_free ? 0 : 1, (const float*)c->embed, c->norms, c->d,
                        c->md.rms_eps, c->h, (float*)c->x, c->U, c->PB, c->SB, c->rope, c->hd / 2,
@@ -1913,7 +1930,7 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
       const int nb = (c->V + 127) / 128;
       nchunks = nb;
       PROF_B(c);
-      hipLaunchKernelGGL((k_gemm_bf16_lds<2, 8, 64, 2, 0>), dim3(nb, 1, 1), dim3(256), 0, st,
+      launch_k(c, st, (k_gemm_bf16_lds<2, 8, 64, 2, 0>), dim3(nb, 1, 1), dim3(256), 0,
                          (const uint16_t*)c->x, (const uint16_t*)c->lm_head, (void*)nullptr, c->rows_M, c->V,
                          c->d, c->d, (int64_t)0,
                          SampleArgs{c->rows, (const CtlParams*)c->cp_dev, logits, c->samp_best, c->samp_idx, S});
@@ -1926,13 +1943,13 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
       gemm(c, c->x, c->lm_head, c->rows_M, S, c->V, c->d, sp, 1);
       PROF_E(c, kPGemmLM, c->V, c->d);
       PROF_B(c);
-      hipLaunchKernelGGL(k_sample_partial, dim3(std::min(S * kSampleChunks, 2048)), dim3(256), 0, st,
+      launch_k(c, st, k_sample_partial, dim3(std::min(S * kSampleChunks, 2048)), dim3(256), 0,
                          c->rows_M, (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, c->ws, c->V,
                          (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, c->samp_best, c->samp_idx);
       PROF_E(c, kPSampleP, c->V, 0);
       if (logits) {
         PROF_B(c);
-        hipLaunchKernelGGL(k_copy_logits, dim3(64, S), dim3(256), 0, st, c->ctl, c->rows, c->ws, c->V,
+        launch_k(c, st, k_copy_logits, dim3(64, S), dim3(256), 0, c->ctl, c->rows, c->ws, c->V,
                            logits);
         PROF_E(c, kPCopy, c->V, 0);
       }
@@ -1941,7 +1958,7 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
   PROF_B(c);
   // chunk winners: [row][kSampleChunks] from k_sample_partial, [chunk][S] from the fused LM head
   const bool fused = !model_free && c->md.dtype == SARA_BF16;
-  hipLaunchKernelGGL(k_sample_final, dim3(std::min(S, 1024)), dim3(256), 0, st, c->ctl, c->rows,
+  launch_k(c, st, k_sample_final, dim3(std::min(S, 1024)), dim3(256), 0, c->ctl, c->rows,
                      c->samp_best, c->samp_idx, nchunks, fused ? S : 1, fused ? 1 : nchunks, forced, c->flen,
                      model_free,
                      (const CtlParams*)c->cp_dev, c->p, c->out_tok, c->samp_tok, c->slot_gen, c->slot_hash, c->fin,
@@ -2012,7 +2029,7 @@ int launch_gumbel_check(double* h_out, hipStream_t st) {
 // Tiled copy of a row-major bf16 weight [rows][K] (rows a multiple of 16)
 // into dst, source tile j going to destination tile j * tile_mul + tile_add.
 int launch_tile_weights(sara_ctx* c, const void* src, void* dst, int rows, int K, int tile_mul, int tile_add) {
-  hipLaunchKernelGGL(k_tile_weights, dim3(2048), dim3(256), 0, c->stream, (const uint16_t*)src, (uint16_t*)dst,
+  launch_k(c, c->stream, k_tile_weights, dim3(2048), dim3(256), 0, (const uint16_t*)src, (uint16_t*)dst,
                      rows / 16, K, tile_mul, tile_add);
   return SARA_OK;
 }
@@ -2020,7 +2037,7 @@ int launch_tile_weights(sara_ctx* c, const void* src, void* dst, int rows, int K
 // Rows of heads head_off.. of a q, k or v weight ([n_rows][K], natural
 // order) into the fused q|k|v tiles in rotation-pair order.
 int launch_tile_weights_pairs(sara_ctx* c, const void* src, void* dst, int n_rows, int K, int head_off) {
-  hipLaunchKernelGGL(k_tile_weights_pairs, dim3(2048), dim3(256), 0, c->stream, (const uint16_t*)src,
+  launch_k(c, c->stream, k_tile_weights_pairs, dim3(2048), dim3(256), 0, (const uint16_t*)src,
                      (uint16_t*)dst, n_rows, K, head_off, c->hd);
   return SARA_OK;
 }
@@ -2039,7 +2056,7 @@ int launch_convert_norms(sara_ctx* c, const void* const* w) {
     else src = w[1 + 9 * (l / 2) + ((l & 1) ? 5 : 0)];
     float* dst = c->norms + (size_t)l * d;
     if (c->md.dtype == SARA_BF16)
-      hipLaunchKernelGGL(k_norm_to_f32_bf16, dim3((d + 255) / 256), dim3(256), 0, c->stream,
+      launch_k(c, c->stream, k_norm_to_f32_bf16, dim3((d + 255) / 256), dim3(256), 0,
                          (const uint16_t*)src, dst, d);
     else {
       hipError_t e = hipMemcpyAsync(dst, src, sizeof(float) * d, hipMemcpyDeviceToDevice, c->stream);

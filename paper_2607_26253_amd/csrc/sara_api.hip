@@ -39,18 +39,19 @@ const char* const kProfNames[kPNumClasses] = {
     "k_embed_norm", "k_sample_partial", "k_sample_final", "k_decode_rows", "k_copy_logits", "k_qkv_rope",
     ".gemm[q|k|v]", ".gemm[o]", ".gemm[gate|up]", ".gemm[down]", ".gemm[lm_head]"};
 
+// prof_begin reserves an event pair for the next kernel launch; launch_k
+// hands it to hipExtLaunchKernelGGL, which stamps the kernel's own start and
+// end; prof_end files the launch under its class.
 void prof_begin(sara_ctx* c) {
   if (c->prof_next_event + 2 > (int)c->prof_events.size()) return;
-  (void)hipEventRecord(c->prof_events[c->prof_next_event], c->stream);
-  c->prof_next_event += 1;
+  c->prof_pending = c->prof_next_event;
+  c->prof_next_event += 2;
 }
 
 void prof_end(sara_ctx* c, int cls, int N, int K) {
-  if (c->prof_next_event + 1 > (int)c->prof_events.size()) return;
-  int e0 = c->prof_next_event - 1;
-  (void)hipEventRecord(c->prof_events[c->prof_next_event], c->stream);
-  c->prof_recs.push_back({cls, N, K, e0, c->prof_next_event});
-  c->prof_next_event += 1;
+  if (c->prof_last >= 0) c->prof_recs.push_back({cls, N, K, c->prof_last, c->prof_last + 1});
+  c->prof_last = -1;
+  c->prof_pending = -1;
 }
 
 // Waits for the recorded events and adds elapsed time and algorithmic bytes

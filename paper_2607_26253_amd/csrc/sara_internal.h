@@ -159,6 +159,8 @@ struct sara_ctx {
   std::vector<hipEvent_t> prof_events;
   std::vector<ProfRec> prof_recs;
   int prof_next_event = 0;
+  int prof_pending = -1;          // event pair reserved for the next launch (-1: none)
+  int prof_last = -1;             // event pair of the last profiled launch
   std::vector<sara_kernel_profile> prof_tot;
   sara::CtlParams cp;              // host copy
   sara::CtlParams* cp_dev = nullptr;
