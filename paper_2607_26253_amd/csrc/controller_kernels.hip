@@ -115,6 +115,16 @@ __global__ __launch_bounds__(kCtlThreads) void k_decide(Ctl* __restrict__ ctl, c
   }
   __threadfence_block();
   __syncthreads();
+  // a prompt becomes quiescent only when one of its rollouts finishes (a
+  // drawn prompt starts with n0 in flight, a continuing one with its new
+  // rollouts), so a step without finishes decides nothing
+  if (s_nfin == 0) {
+    if (tid == 0) {
+      ctl->tokens += ctl->M;
+      ctl->dirty = 0;
+    }
+    return;
+  }
   const int next_uid = ctl->next_uid;
   const int64_t dec_base = ctl->n_dec;
   // decisions, ascending uid

@@ -1157,13 +1157,21 @@ __device__ __forceinline__ void qkv_rope_mblock(const uint16_t* __restrict__ X, 
                                                          __builtin_bit_cast(bf16x8, sg.x[t]), acc[t], 0, 0, 0);
     }
   };
-  int base0 = -D;
-  asm volatile("" : "+s"(base0));       // opaque start: the first (load-only) trip stays in the loop
-  for (int base = base0; base < KS; base += D) {
+  if constexpr (D == KS) {
+    // every k step in flight at once: exactly KS loads, then the MFMAs
 #pragma unroll
-    for (int j = 0; j < D; ++j) {
-      load(st[(j + D - 1) % D], base + j + D - 1);
-      if (base >= 0) consume(st[j], base + j);
+    for (int j = 0; j < KS; ++j) load(st[j], j);
+#pragma unroll
+    for (int j = 0; j < KS; ++j) consume(st[j], j);
+  } else {
+    int base0 = -D;
+    asm volatile("" : "+s"(base0));     // opaque start: the first (load-only) trip stays in the loop
+    for (int base = base0; base < KS; base += D) {
+#pragma unroll
+      for (int j = 0; j < D; ++j) {
+        load(st[(j + D - 1) % D], base + j + D - 1);
+        if (base >= 0) consume(st[j], base + j);
+      }
     }
   }
 #pragma unroll
