@@ -319,7 +319,7 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   const size_t fb = (size_t)c->ffn * d * E;
   hipError_t e = cp(c->embed, d_weights[0], (size_t)c->V * d * E);
   if (md->dtype == SARA_BF16) {
-    // GEMM weights in the fragment-major tiled layout of the bf16 GEMM
+    // GEMM weights in the k-block-major fragment layout of the bf16 GEMM (wtiled_index)
     const int kvr = c->hkv * c->hd;
     for (int l = 0; l < c->L && e == hipSuccess; ++l) {
       const void* const* w = d_weights + 1 + 9 * l;
@@ -327,14 +327,14 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
       launch_tile_weights_pairs(c, w[1], c->w_qkv[l], c->qdim, d, 0);
       launch_tile_weights_pairs(c, w[2], c->w_qkv[l], kvr, d, c->hq);
       launch_tile_weights_pairs(c, w[3], c->w_qkv[l], kvr, d, c->hq + c->hkv);
-      launch_tile_weights(c, w[4], c->w_o[l], d, c->qdim, 1, 0);
+      launch_tile_weights(c, w[4], c->w_o[l], d, c->qdim, 1, 0, d);
       // gate and up tiles interleaved (gate tile j -> 2j, up tile j -> 2j + 1) for the SwiGLU epilogue
-      launch_tile_weights(c, w[6], c->w_gu[l], c->ffn, d, 2, 0);
-      launch_tile_weights(c, w[7], c->w_gu[l], c->ffn, d, 2, 1);
-      launch_tile_weights(c, w[8], c->w_d[l], d, c->ffn, 1, 0);
+      launch_tile_weights(c, w[6], c->w_gu[l], c->ffn, d, 2, 0, 2 * c->ffn);
+      launch_tile_weights(c, w[7], c->w_gu[l], c->ffn, d, 2, 1, 2 * c->ffn);
+      launch_tile_weights(c, w[8], c->w_d[l], d, c->ffn, 1, 0, d);
       e = hipGetLastError();
     }
-    launch_tile_weights(c, d_weights[2 + 9 * c->L], c->lm_head, c->V, d, 1, 0);
+    launch_tile_weights(c, d_weights[2 + 9 * c->L], c->lm_head, c->V, d, 1, 0, c->V);
     if (e == hipSuccess) e = hipGetLastError();
   } else {
     for (int l = 0; l < c->L && e == hipSuccess; ++l) {

@@ -200,7 +200,8 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
                        uint32_t feos, int32_t* tok, hipStream_t st);
 int launch_convert_norms(sara_ctx* c, const void* const* w);
 int launch_gumbel_check(double* h_out, hipStream_t st);
-int launch_tile_weights(sara_ctx* c, const void* src, void* dst, int rows, int K, int tile_mul, int tile_add);
+int launch_tile_weights(sara_ctx* c, const void* src, void* dst, int rows, int K, int tile_mul, int tile_add,
+                        int dst_rows);
 int launch_tile_weights_pairs(sara_ctx* c, const void* src, void* dst, int n_rows, int K, int head_off);
 
 // ---------------------------------------------------------------------------
