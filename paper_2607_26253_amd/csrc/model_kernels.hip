@@ -145,10 +145,56 @@ __global__ __launch_bounds__(256) void k_decode_embed(const Ctl* __restrict__ ct
     int32_t* __restrict__ rows_M, int do_embed, const T* __restrict__ embed,
     const float* __restrict__ w, int d, float eps, float* __restrict__ h, T* __restrict__ x,
     int U, int PB, int SB, const float2* __restrict__ rope, int half, float2* __restrict__ row_rope,
-    int x_tiled) {
+    int x_tiled, AttnItem* __restrict__ items, int32_t* __restrict__ n_items, int spg) {
   __shared__ float red[4];
+  __shared__ int scan[256];
   const int M = ctl->done ? 0 : ctl->M;
   if (blockIdx.x == 0 && threadIdx.x == 0) *rows_M = M;
+  if (items != nullptr && blockIdx.x == gridDim.x - 1) {
+    // The decode attention's work list for this step (the same for every
+    // layer): the context splits of spg pages of every row, row-major.
+    // Thread t lists rows [t * per, (t + 1) * per) at the exclusive prefix
+    // sum of the earlier threads' split counts.
+    const int per = (M + 255) / 256;
+    const int i0 = min(M, (int)threadIdx.x * per), i1 = min(M, i0 + per);
+    auto item_of = [&](int i, int cc) {
+      const int s = active[i];
+      const int u = slot_uid[s], g = slot_gen[s];
+      AttnItem it;
+      it.i = i;
+      it.c = cc;
+      it.kv0 = u * PB;
+      it.kv1 = U * PB + s * SB;
+      it.pl = off[u + 1] - off[u] - 1;    // context P + g exceeds the P - 1 prompt positions
+      it.vcnt = g + 1;
+      it.pad0 = it.pad1 = 0;
+      return it;
+    };
+    auto splits_of = [&](const AttnItem& it) {
+      const int nch = ((it.pl + 15) >> 4) + ((it.vcnt + 15) >> 4);
+      return (nch + spg - 1) / spg;
+    };
+    int cnt = 0;
+    for (int i = i0; i < i1; ++i) cnt += splits_of(item_of(i, 0));
+    scan[threadIdx.x] = cnt;
+    __syncthreads();
+    for (int o = 1; o < 256; o <<= 1) {
+      const int v = (int)threadIdx.x >= o ? scan[threadIdx.x - o] : 0;
+      __syncthreads();
+      scan[threadIdx.x] += v;
+      __syncthreads();
+    }
+    int at = scan[threadIdx.x] - cnt;
+    for (int i = i0; i < i1; ++i) {
+      AttnItem it = item_of(i, 0);
+      const int ns = splits_of(it);
+      for (int cc = 0; cc < ns; ++cc) {
+        it.c = cc;
+        items[at++] = it;
+      }
+    }
+    if (threadIdx.x == 255) *n_items = scan[255];
+  }
   for (int i = blockIdx.x; i < M; i += gridDim.x) {
     const int s = active[i];
     const int u = slot_uid[s], j = slot_j[s], g = slot_gen[s];
@@ -1264,12 +1310,14 @@ __global__ __launch_bounds__(256) void k_qkv_rope(const uint16_t* __restrict__ X
 
 // Decode attention (bf16, MFMA) over the KV pages, q read from qbuf (the
 // q|k|v kernel has already rotated q and appended this position's k and v).
-// Item = (split c, row i, KV head g), split-major; a split is kDecPages
-// pages and wave w owns pages w, w + 4, .. of it, all K and V loads issued
-// before any compute, so a split costs one HBM round trip.  Page ids come
-// from the row's two KV extents (kv0 + e: shared prompt pages, kv1 + e:
-// private pages), so no block-table read sits between the row descriptor
-// and the page loads.  Per page (16 tokens):
+// Work item = (entry e of the step's work list, KV head g): entry e names a
+// row and one of its context splits of kDecPages pages; wave w owns pages
+// w, w + 4, .. of the split, all K and V loads issued before any compute, so
+// a split costs one HBM round trip.  The entry carries the row's two KV
+// extents (kv0 + e: shared prompt pages, kv1 + e: private pages), so the
+// page loads wait on that one load only; the grid is the number of blocks
+// that are resident at once, so up to that many items all run in one
+// round.  Per page (16 tokens):
 //   S^T = K q^T  (v_mfma_f32_16x16x32_bf16; G <= 8 query heads padded to 16;
 //                 lane (token l%16, k-group l/16) of K meets head l%16 of q
 //                 over the same HD/4 dims, so the k order inside the MFMA is moot)
@@ -1282,8 +1330,8 @@ __global__ __launch_bounds__(256) void k_qkv_rope(const uint16_t* __restrict__ X
 // its normalised output to `out` ([row][hq][HD], bf16); other rows leave a
 // partial per split for k_attn_combine.
 template <int HD>
-__global__ __launch_bounds__(256, 2) void k_attn_dec(const int32_t* __restrict__ M_ptr,
-    const RowDesc* __restrict__ rows, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
+__global__ __launch_bounds__(256, 2) void k_attn_dec(const AttnItem* __restrict__ items,
+    const int32_t* __restrict__ n_items, int cap, const uint16_t* __restrict__ kc, const uint16_t* __restrict__ vc,
     int layer, int64_t n_blocks, int hq, int hkv, int n_splits, float scale,
     const uint16_t* __restrict__ qb, float* __restrict__ part, uint16_t* __restrict__ out) {
   typedef short short4_ __attribute__((ext_vector_type(4)));
@@ -1291,14 +1339,17 @@ __global__ __launch_bounds__(256, 2) void k_attn_dec(const int32_t* __restrict__
   constexpr int DPL = HD / 4, NCC = HD / 32, NT = HD / 16, PPW = kDecPpw, SPG = kDecPages;
   __shared__ float m_w[4][16], l_w[4][16];
   __shared__ float o_w[4][16][HD + 1];
-  const int M = *M_ptr;
-  const int total = M * hkv * n_splits;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int row = lane & 15, grp = lane >> 4;
   const int G = hq / hkv;
-  for (int item = blockIdx.x; item < total; item += gridDim.x) {
-    const int c = item / (M * hkv);
-    const int i = (item - c * M * hkv) / hkv, g = item % hkv;
+  for (int item = blockIdx.x; item < cap * hkv; item += gridDim.x) {
+    // the list length and the entry are loaded together (the loop bound
+    // keeps the entry index below the list's capacity)
+    const int n = *n_items;
+    const int4 e0 = *(const int4*)&items[item / hkv].i;
+    const int2 e1 = *(const int2*)&items[item / hkv].pl;
+    if (item >= n * hkv) break;
+    const int i = e0.x, c = e0.y, g = item % hkv;
     // q operand (head `row` of this KV group, zero beyond G): independent of
     // the row descriptor, loaded first
     uint4 qv[NCC];
@@ -1312,11 +1363,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_dec(const int32_t* __restrict__
         for (int cc = 0; cc < NCC; ++cc) qv[cc] = make_uint4(0, 0, 0, 0);
       }
     }
-    const RowDesc r = rows[i];
-    const int ctx = r.pos + 1;
-    const int pl = min(ctx, r.plen);                      // prompt positions attended
+    const int kv0 = e0.z, kv1 = e0.w;
+    const int pl = e1.x;                                   // prompt positions attended
     const int pc = (pl + 15) >> 4;                         // prompt pages
-    const int vcnt = ctx - pl;                             // private positions (>= 1)
+    const int vcnt = e1.y;                                 // private positions (>= 1)
     const int nch = pc + ((vcnt + 15) >> 4);
     const int ch0 = c * SPG;
     if (ch0 >= nch) continue;
@@ -1331,7 +1381,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_dec(const int32_t* __restrict__
       if (cv < pc) n = min(16, pl - 16 * cv);
       else n = min(16, vcnt - 16 * (cv - pc));
       pg[p].n = (ch < ch1) ? n : 0;
-      const int blk = (cv < pc) ? r.kv0 + cv : r.kv1 + (cv - pc);
+      const int blk = (cv < pc) ? kv0 + cv : kv1 + (cv - pc);
       const size_t pgi = ((size_t)layer * n_blocks + blk) * hkv + g;
       const u32x4* kp = (const u32x4*)(kc + (pgi * kBlockTok + row) * HD + DPL * grp);
 #pragma unroll
@@ -1824,8 +1874,19 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
 #undef SARA_QKV
       PROF_E(c, kPQkvRope, c->nqkv, d);
       PROF_B(c);
-      const int dg = (int)std::min<int64_t>((int64_t)M_cap * c->hkv * c->dec_splits_max, 2048);
-      launch_k(c, st, (k_attn_dec<HD>), dim3(dg), dim3(256), 0, M_ptr, c->rows, (const uint16_t*)c->kc,
+      if (c->attn_dec_grid == 0) {
+        // blocks resident at once: every item of a list that short runs in one round
+        int per_cu = 0, dev = 0, n_cu = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_attn_dec<HD>, 256, 0) != hipSuccess ||
+            hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+          per_cu = 2, n_cu = 256;
+        c->attn_dec_grid = std::max(1, per_cu) * std::max(1, n_cu);
+      }
+      const int cap = M_cap * c->dec_splits_max;
+      const int dg = (int)std::min<int64_t>((int64_t)cap * c->hkv, c->attn_dec_grid);
+      launch_k(c, st, (k_attn_dec<HD>), dim3(dg), dim3(256), 0, (const AttnItem*)c->attn_items,
+                         (const int32_t*)c->attn_nitems, cap, (const uint16_t*)c->kc,
                          (const uint16_t*)c->vc, l, c->n_blocks, c->hq, c->hkv, c->dec_splits_max,
                          1.0f / sqrtf((float)HD), (const uint16_t*)c->qbuf, c->attn_part, (uint16_t*)x);
       PROF_E(c, kPAttn, 0, 0);
@@ -1940,13 +2001,14 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
                        c->slot_j, c->slot_gen, c->tok, c->off, c->out_tok, c->k, c->ad.max_new, c->rows,
                        c->rows_M, model_free ? 0 : 1, (const uint16_t*)c->embed, c->norms, c->d,
                        c->md.rms_eps, c->h, (uint16_t*)c->x, c->U, c->PB, c->SB, c->rope, c->hd / 2,
-                       c->row_rope, 1);
+                       c->row_rope, 1, model_free ? (AttnItem*)nullptr : c->attn_items, c->attn_nitems,
+                       kDecPages);
   else
     launch_k(c, st, k_decode_embed<float>, dim3(eg), dim3(256), 0, c->ctl, c->active, c->slot_uid,
                        c->slot_j, c->slot_gen, c->tok, c->off, c->out_tok, c->k, c->ad.max_new, c->rows,
                        c->rows_M, model_free ? 0 : 1, (const float*)c->embed, c->norms, c->d,
                        c->md.rms_eps, c->h, (float*)c->x, c->U, c->PB, c->SB, c->rope, c->hd / 2,
-                       c->row_rope, 0);
+                       c->row_rope, 0, (AttnItem*)nullptr, c->attn_nitems, kDecPages);
   PROF_E(c, kPEmbed, c->d, 0);
   int nchunks = kSampleChunks;
   if (!model_free) {

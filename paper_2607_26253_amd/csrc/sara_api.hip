@@ -249,6 +249,8 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   ALLOC(c->btab, sizeof(int32_t) * (size_t)(c->S + c->U) * c->MAXB);
   ALLOC(c->rope, sizeof(float2) * (size_t)c->max_pos * (c->hd / 2));
   ALLOC(c->row_rope, sizeof(float2) * (size_t)c->S * (c->hd / 2));
+  ALLOC(c->attn_items, sizeof(AttnItem) * (size_t)c->S * c->dec_splits_max);
+  ALLOC(c->attn_nitems, sizeof(int32_t) * 4);
   // prompt pool
   c->tok_cap = (int64_t)c->U * ad->max_prompt;
   ALLOC(c->tok, sizeof(int32_t) * c->tok_cap);

@@ -56,6 +56,14 @@ struct RowDesc {
   int32_t kv1;
 };
 
+// One work item of the decode attention: context split c of decode row i,
+// with the row's page extents and segment lengths, so that an attention
+// block needs no further load before its page loads.
+struct AttnItem {
+  int32_t i, c, kv0, kv1;   // row, split, page extents (as in RowDesc)
+  int32_t pl, vcnt, pad0, pad1;  // prompt positions attended, private positions
+};
+
 // Parameters every controller kernel reads.
 struct CtlParams {
   int32_t B, k, n0, commit_min, U, S, mode, bits, max_new, PB, SB, MAXB, eos, Qcap;
@@ -100,6 +108,9 @@ struct sara_ctx {
   int32_t* btab = nullptr;
   float2* rope = nullptr;         // [max_pos][hd/2] (cos, sin)
   float2* row_rope = nullptr;     // [S][hd/2] (cos, sin) at each decode row's position
+  sara::AttnItem* attn_items = nullptr; // [S * dec_splits_max] decode attention work list of the step
+  int32_t* attn_nitems = nullptr; // its length
+  int attn_dec_grid = 0;          // blocks of the decode attention that are resident at once
 
   // prompt pool (library copies)
   int32_t* tok = nullptr;

@@ -173,14 +173,20 @@ def _model_free_case(cfg, U_tokens_seed=3):
 
 @pytest.mark.parametrize("name,mode", [("qwen1p5b_shape", "sara"), ("long_ragged_1p5b", "sara"),
                                        ("pool_3b", "sara"), ("pool_3b", "fixed_k"),
-                                       ("qwen3b_shape", "sara")])
+                                       ("qwen3b_shape", "sara"),
+                                       ("qwen1p5b_shape", "commit_min=2"), ("qwen1p5b_shape", "commit_min=4")])
 def test_controller_full_size_model_free(torch_cuda, name, mode):
     """Full-size allocation parameters of each workload; tokens from a table
     (decoder skipped), so the controller, hash reward and termination are
-    checked bit-exactly against the oracle's event simulation."""
+    checked bit-exactly against the oracle's event simulation.  The
+    commit_min cases are the early-commit variant (commit at the first mix,
+    Theorem 2's proof, and the floor of 4 of the commit-floor ablation): groups
+    of 2..8 rollouts, so the GRPO advantages run over variable group sizes."""
     full = W.get_config(name)
     if mode == "fixed_k":
         full = W.fixed_k_variant(full)
+    elif mode.startswith("commit_min="):
+        full["alloc"]["commit_min"] = int(mode.split("=")[1])
     cfg = W.get_config("tiny_f32")
     cfg["alloc"] = dict(full["alloc"])
     cfg["alloc"]["max_prompt"] = 32
@@ -211,6 +217,9 @@ def test_controller_full_size_model_free(torch_cuda, name, mode):
     off, r, adv = gpu["adv"]
     assert np.array_equal(off, ora["grpo_offsets"])
     assert np.allclose(adv, ora["advantages"], rtol=1e-6, atol=1e-6)
+    if mode.startswith("commit_min="):
+        sizes = np.diff(off)
+        assert sizes.size == 0 or sizes.min() >= a["commit_min"]
     ctx.close()
 
 

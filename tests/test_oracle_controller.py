@@ -228,3 +228,63 @@ def test_fixed_k_mode_is_uniform_sampling():
     sara = C.simulate(alloc(B=64, budget_N=3072), U, synthetic(p))
     for (u, j), (L, r, _, _) in sara["rollout"].items():
         assert res["rollout"][(u, j)][1] == r
+
+
+def expected_rollouts(g, m, n_a):
+    """Eq. EN generalised to a commit floor m <= n_a: a prompt stops at
+    N = min(max(T_mix, m), n_a), with Pr[T_mix > n] = g^n + (1-g)^n (n >= 1),
+    so E[N] = m + sum_{n=m}^{n_a-1} (g^n + (1-g)^n); m = 2 is Eq. EN itself."""
+    return m + sum(g ** n + (1 - g) ** n for n in range(m, n_a))
+
+
+@pytest.mark.parametrize("g", [0.5, 0.2, 0.05])
+def test_early_commit_expected_rollouts_eq_en(g):
+    """Theorem 2 (Eq. EN): with the commit floor at the first mix (commit_min
+    = 2) and a Bernoulli(g) reward stream, the mean rollouts per drawn prompt
+    is 1 + sum_{n=1}^{n_a-1} (g^n + (1-g)^n), n_a = k - floor(tau (k+1)) = 4."""
+    U = 20000
+    p = np.full(U, g)
+    a = alloc(commit_min=2, B=10 ** 6, budget_N=10 ** 7, n_slots=4096)
+    res = C.simulate(a, U, synthetic(p, seed=11))
+    assert res["drawn"] == U
+    n_a = 8 - math.floor(0.45 * 9)
+    assert n_a == 4
+    en = 1 + sum(g ** n + (1 - g) ** n for n in range(1, n_a))
+    assert en == pytest.approx(expected_rollouts(g, 2, n_a))
+    # N takes values in {2, 3, 4}: variance <= 1, so 5 sigma <= 5 / sqrt(U)
+    assert abs(res["rollouts"] / U - en) < 5 / math.sqrt(U)
+    # a prompt commits iff it mixes by n_a, the moment it mixes
+    pc = 1 - (g ** n_a + (1 - g) ** n_a)
+    assert abs(res["n_committed"] / U - pc) < 5 * math.sqrt(pc * (1 - pc) / U)
+    for u in range(U):
+        n, s = res["n_done"][u], res["successes"][u]
+        if res["status"][u] == C.COMMITTED:
+            assert 1 <= s <= n - 1 and n <= n_a
+            # the first n - 1 outcomes were all the same (committed at the first mix)
+            outs = [r for _, r in synthetic(p, seed=11)([(u, j) for j in range(n)])]
+            assert len(set(outs[:-1])) == 1 and outs[-1] != outs[0]
+        else:
+            assert n == n_a and s in (0, n)
+    check_invariants(a, res, U)
+
+
+@pytest.mark.parametrize("m", [2, 3, 4])
+def test_commit_floor_mixture_rollouts(m):
+    """Commit floor m under the survey's success-rate mixture: E[N] =
+    m + sum_{n=m}^{n_a-1} E[g^n + (1-g)^n]; commit probability 1 - E[g^4 + (1-g)^4]
+    for every floor m <= n_a (mixing is absorbing, the abandonment point is unchanged)."""
+    U = 20000
+    p = mixture_p(U, 21)
+    a = alloc(commit_min=m, B=10 ** 6, budget_N=10 ** 7, n_slots=4096)
+    res = C.simulate(a, U, synthetic(p, seed=5))
+    n_a = 4
+    en = m + sum(moment(n, 0) for n in range(m, n_a))
+    assert abs(res["rollouts"] / U - en) < 5 * 2 / math.sqrt(U)
+    pc = 1 - moment(4, 0)
+    assert abs(res["n_committed"] / U - pc) < 5 * math.sqrt(pc * (1 - pc) / U)
+    # every committed group has between m and n_a members: variable group sizes
+    sizes = [res["n_done"][u] for u in range(U) if res["status"][u] == C.COMMITTED]
+    assert min(sizes) >= m and max(sizes) <= n_a
+    if m < n_a:
+        assert len(set(sizes)) > 1
+    check_invariants(a, res, U)
