@@ -46,6 +46,8 @@ enum { SARA_MODE_SARA = 0, SARA_MODE_FIXED_K = 1 };
 enum { SARA_COMMIT = 1, SARA_ABANDON = 2, SARA_CONTINUE = 3 };
 /* per-prompt status */
 enum { SARA_UNDRAWN = 0, SARA_ACTIVE = 1, SARA_COMMITTED = 2, SARA_ABANDONED = 3 };
+/* bits of the device error word (sara_step_stats.error) */
+enum { SARA_DEVERR_WARM_ID = 1 };   /* a warm-start prompt id outside [0, n_store) */
 
 /* Decoder shape.  Pre-norm GQA decoder: RMSNorm, rotate-half RoPE, SwiGLU,
  * untied LM head, no biases.  head_dim in {64, 128}; n_heads a multiple of
@@ -168,6 +170,38 @@ int sara_query(sara_ctx* ctx, sara_step_stats* out);
 /* Build the CSR of committed groups (ascending uid, rollouts in j order) and
  * compute their GRPO advantages with grpo_group_advantages.  Enqueued. */
 int sara_finish_step(sara_ctx* ctx, float eps);
+
+/* History warm start (implementation details, "defaults and history
+ * warm-start": each prompt carries its posterior across steps with an
+ * exponential decay lambda).  For a finite prompt set revisited across
+ * allocation steps, set prompt p keeps pseudo-counts (a_p, b_p) >= 0.
+ *
+ * sara_set_warm_start: from the next sara_begin_step on, pool prompt u is
+ * set prompt d_ids[u] and starts from the prior Beta(alpha0 + a_{ids[u]},
+ * beta0 + b_{ids[u]}) in place of Beta(alpha0, beta0): its p_eff, its
+ * decisions (Eq. decide on the posterior Beta(alpha0 + a + s,
+ * beta0 + b + n - s)) and the priority of its probes use that prior.
+ *   d_ids  [pool_U] int32, distinct values in [0, n_store)
+ *   d_a, d_b [n_store] fp64 pseudo-counts
+ * All three stay owned by the caller and must stay valid while warm start is
+ * on: every sara_begin_step reads d_ids, d_a and d_b (update the ids between
+ * steps to move the pool over the set), sara_warm_start_update writes d_a
+ * and d_b.  d_ids == NULL turns warm start off (back to Beta(alpha0, beta0)).
+ * Errors: SARA_EINVAL for a null context, or non-null d_ids with null d_a /
+ * d_b or n_store < 1.  An id outside [0, n_store) is found on the device:
+ * that prompt falls back to Beta(alpha0, beta0) and the step's device error
+ * word gets SARA_DEVERR_WARM_ID (sara_query then returns SARA_EDEVICE).
+ * Duplicate ids are not detected; their count updates race. */
+int sara_set_warm_start(sara_ctx* ctx, const int32_t* d_ids, double* d_a, double* d_b, int32_t n_store);
+
+/* After a step's decode loop has ended (the step is done): for every set
+ * prompt p, a_p <- lambda (a_p + s_p) and b_p <- lambda (b_p + n_p - s_p),
+ * where n_p and s_p are the rollouts and successes the step gave the pool
+ * prompt with id p (0 and 0 if the step did not draw it).  lambda in [0, 1]:
+ * 0 forgets (every step starts cold), 1 keeps every outcome.  Enqueued.
+ * Errors: SARA_EINVAL for a null context or lambda outside [0, 1];
+ * SARA_ESTATE when no warm start is set or no step has begun. */
+int sara_warm_start_update(sara_ctx* ctx, double lambda);
 
 /* Copy results to host (synchronises).  Any pointer may be NULL.
  *   h_tokens  [pool_U*k][max_new] int32 appended tokens (-1 past the end)

@@ -30,14 +30,20 @@ end     when no prompt is active (then no slot is busy and Q is empty).
 Budget reading: the paper's "budget left" and safety cap are unspecified;
 k rollouts are reserved per drawn prompt and k - n refunded when it is
 decided, so rollouts spent never exceed N.
+
+History warm start (implementation details, "defaults and history
+warm-start"): `priors` gives each pool prompt its own Beta(alpha0_u,
+beta0_u) prior (see warm.py); its p_eff, decisions and the priority of its
+probes then use that prior in place of Beta(alpha0, beta0).
 """
 from .predictor import ABANDON, COMMIT, CONTINUE, decide, p_eff, priority_key
 
 UNDRAWN, ACTIVE, COMMITTED, ABANDONED = 0, 1, 2, 3
 
 
-def simulate(alloc: dict, U: int, outcomes):
+def simulate(alloc: dict, U: int, outcomes, priors=None):
     """outcomes(list[(uid, j)]) -> list[(length, reward)] for newly started rollouts.
+    priors: optional (alpha0_u, beta0_u) sequences of length U (warm start).
 
     Returns a dict with the decision / draw / assignment / finish logs and the
     per-prompt and per-rollout results."""
@@ -54,7 +60,12 @@ def simulate(alloc: dict, U: int, outcomes):
     slots = [None] * S                  # (uid, j, finish step, reward, length)
     rollout = {}                        # (uid, j) -> (length, reward, start, slot)
     log_dec, log_draw, log_asg, log_fin = [], [], [], []
-    prior = p_eff(0, 0, k, a0, b0)
+    if priors is None:
+        pa, pb = [a0] * U, [b0] * U
+    else:
+        pa, pb = [float(x) for x in priors[0]], [float(x) for x in priors[1]]
+        assert len(pa) == U and len(pb) == U
+    prior = [p_eff(0, 0, k, pa[u], pb[u]) for u in range(U)]
 
     def refill(start):
         nonlocal budget, next_uid, nA
@@ -64,7 +75,7 @@ def simulate(alloc: dict, U: int, outcomes):
             status[u] = ACTIVE
             budget -= k
             nA += 1
-            pe[u] = prior
+            pe[u] = prior[u]
             n_iss[u] = n0
             infl[u] = n0
             Q.extend((u, j) for j in range(n0))
@@ -101,7 +112,7 @@ def simulate(alloc: dict, U: int, outcomes):
             if status[u] != ACTIVE or infl[u] != 0:
                 continue
             n, s = n_done[u], succ[u]
-            d, pv, more = decide(n, s, k, cm, tau, a0, b0)
+            d, pv, more = decide(n, s, k, cm, tau, pa[u], pb[u])
             pe[u] = pv
             log_dec.append((t, u, d, n, s, pv))
             if d == COMMIT:

@@ -24,7 +24,7 @@ EXPORTED = ["sara_init", "sara_begin_step", "sara_decode_step", "sara_posterior_
             "sara_refill", "sara_run", "sara_query", "sara_finish_step", "sara_read_rollouts",
             "sara_read_logs", "sara_read_advantages", "sara_peff_batch", "grpo_group_advantages",
             "sara_sample_logits", "sara_gumbel_fast_max_error", "sara_set_profiling", "sara_reset_profile",
-            "sara_read_profile",
+            "sara_read_profile", "sara_set_warm_start", "sara_warm_start_update",
             "sara_destroy",
             "sara_last_error"]
 
@@ -84,6 +84,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "sara_set_profiling": [P, I32],
         "sara_reset_profile": [P],
         "sara_read_profile": [P, ctypes.POINTER(sara_kernel_profile), I32, ctypes.POINTER(I32)],
+        "sara_set_warm_start": [P, P, P, P, I32],
+        "sara_warm_start_update": [P, F64],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -236,6 +238,19 @@ class Sara:
     def sara_finish_step(self, eps=1e-6):
         self._in()
         _check(_lib.sara_finish_step(self.h, float(eps)), "sara_finish_step")
+        self._out()
+
+    def sara_set_warm_start(self, d_ids=None, d_a=None, d_b=None):
+        """History warm start over a prompt set: d_ids [pool_U] int32 (set
+        prompt of each pool prompt), d_a / d_b [n_store] fp64 pseudo-counts,
+        all device tensors kept alive by the caller; d_ids=None turns it off."""
+        n = 0 if d_ids is None else int(d_a.numel())
+        self._warm = (d_ids, d_a, d_b)
+        _check(_lib.sara_set_warm_start(self.h, _ptr(d_ids), _ptr(d_a), _ptr(d_b), n), "sara_set_warm_start")
+
+    def sara_warm_start_update(self, lam):
+        self._in()
+        _check(_lib.sara_warm_start_update(self.h, float(lam)), "sara_warm_start_update")
         self._out()
 
     def sara_set_profiling(self, enable=True):

@@ -73,7 +73,8 @@ __global__ __launch_bounds__(kCtlThreads) void k_decide(Ctl* __restrict__ ctl, c
     int32_t* __restrict__ slot_uid, const int32_t* __restrict__ slot_j,
     int32_t* __restrict__ fin, const int32_t* __restrict__ r_len,
     const int32_t* __restrict__ r_reward, uint64_t* __restrict__ queue,
-    int64_t* __restrict__ log_dec, int64_t* __restrict__ log_fin) {
+    int64_t* __restrict__ log_dec, int64_t* __restrict__ log_fin,
+    const double* __restrict__ prior_a, const double* __restrict__ prior_b) {
   __shared__ int buf[kCtlThreads];
   __shared__ int s_nfin, s_ndec, s_qlen, s_dC, s_dA, s_dAb, s_more;
   __shared__ unsigned long long s_refund;
@@ -137,7 +138,7 @@ __global__ __launch_bounds__(kCtlThreads) void k_decide(Ctl* __restrict__ ctl, c
       pred = 1;
       n = atomicAdd(&n_done[u], 0);
       s = atomicAdd(&succ[u], 0);
-      pe = peff_dev(n, s, cp.k, cp.a0, cp.b0);
+      pe = cp.has_prior ? peff_dev(n, s, cp.k, prior_a[u], prior_b[u]) : peff_dev(n, s, cp.k, cp.a0, cp.b0);
       bool mixed = (s >= 1) && (n - s >= 1);
       if (mixed && n >= cp.commit_min) code = SARA_COMMIT;
       else if (n >= cp.k) code = SARA_ABANDON;
@@ -194,7 +195,7 @@ __global__ __launch_bounds__(kCtlThreads) void k_refill(Ctl* __restrict__ ctl, c
     double* __restrict__ peff, int32_t* __restrict__ slot_uid, int32_t* __restrict__ slot_j,
     int32_t* __restrict__ slot_gen, uint64_t* __restrict__ slot_hash,
     int32_t* __restrict__ active, uint64_t* __restrict__ queue, int32_t* __restrict__ btab,
-    int64_t* __restrict__ log_draw, int64_t* __restrict__ log_asg) {
+    int64_t* __restrict__ log_draw, int64_t* __restrict__ log_asg, const double* __restrict__ prior_p) {
   __shared__ int buf[kCtlThreads];
   __shared__ uint64_t qs[kMaxQueue];
   __shared__ int freel[kMaxSlots];
@@ -233,7 +234,7 @@ __global__ __launch_bounds__(kCtlThreads) void k_refill(Ctl* __restrict__ ctl, c
     status[u] = SARA_ACTIVE;
     n_iss[u] = cp.n0;
     infl[u] = cp.n0;
-    peff[u] = cp.prior;
+    peff[u] = cp.has_prior ? prior_p[u] : cp.prior;
     int64_t* lr = log_draw + (draw_base + e) * 2;
     lr[0] = tnext; lr[1] = u;
   }
@@ -249,7 +250,8 @@ __global__ __launch_bounds__(kCtlThreads) void k_refill(Ctl* __restrict__ ctl, c
     if (e < s_qlen) key = queue[e];
     else if (e < qlen) {
       int q = e - s_qlen;
-      key = queue_key(cp.prior, cp.bits, nu0 + q / cp.n0, q % cp.n0);
+      const int uq = nu0 + q / cp.n0;
+      key = queue_key(cp.has_prior ? prior_p[uq] : cp.prior, cp.bits, uq, q % cp.n0);
     }
     qs[e] = key;
   }
@@ -400,6 +402,55 @@ __global__ __launch_bounds__(kCtlThreads) void k_build_csr(const Ctl* __restrict
 }
 
 // ---------------------------------------------------------------------------
+// history warm start
+// ---------------------------------------------------------------------------
+// Priors of the step's pool from the prompt set's pseudo-counts: pool prompt
+// u is set prompt ids[u] and starts from Beta(a0 + a[ids[u]], b0 + b[ids[u]]);
+// prior_p is p_eff(0, 0) under it (the priority of its probes).  An id
+// outside [0, n_store) sets the device error word and falls back to the
+// global prior.  Runs after k_reset (which clears the error word).
+__global__ void k_warm_priors(Ctl* __restrict__ ctl, const CtlParams* __restrict__ cpp,
+    const int32_t* __restrict__ ids, const double* __restrict__ a, const double* __restrict__ b, int n_store,
+    double* __restrict__ prior_a, double* __restrict__ prior_b, double* __restrict__ prior_p) {
+  const CtlParams cp = *cpp;
+  for (int u = blockIdx.x * blockDim.x + threadIdx.x; u < cp.U; u += gridDim.x * blockDim.x) {
+    const int id = ids[u];
+    double al = cp.a0, be = cp.b0;
+    if (id >= 0 && id < n_store) {
+      al = cp.a0 + a[id];
+      be = cp.b0 + b[id];
+    } else {
+      atomicOr(&ctl->error, SARA_DEVERR_WARM_ID);
+    }
+    prior_a[u] = al;
+    prior_b[u] = be;
+    prior_p[u] = peff_dev(0, 0, cp.k, al, be);
+  }
+}
+
+// After a step: the drawn pool prompts add their outcomes to their set
+// prompt's counts (ids are distinct, so no two threads share an entry) ...
+__global__ void k_warm_add(const Ctl* __restrict__ ctl, const int32_t* __restrict__ ids, int U, int n_store,
+    const int32_t* __restrict__ n_done, const int32_t* __restrict__ succ,
+    double* __restrict__ a, double* __restrict__ b) {
+  const int drawn = min(ctl->next_uid, U);
+  for (int u = blockIdx.x * blockDim.x + threadIdx.x; u < drawn; u += gridDim.x * blockDim.x) {
+    const int id = ids[u];
+    if (id < 0 || id >= n_store) continue;
+    a[id] = a[id] + (double)succ[u];
+    b[id] = b[id] + (double)(n_done[u] - succ[u]);
+  }
+}
+
+// ... then every entry of the set decays by lambda
+__global__ void k_warm_decay(double* __restrict__ a, double* __restrict__ b, int n_store, double lambda) {
+  for (int p = blockIdx.x * blockDim.x + threadIdx.x; p < n_store; p += gridDim.x * blockDim.x) {
+    a[p] = lambda * a[p];
+    b[p] = lambda * b[p];
+  }
+}
+
+// ---------------------------------------------------------------------------
 // host launchers
 // ---------------------------------------------------------------------------
 int launch_reset(sara_ctx* c) {
@@ -412,14 +463,29 @@ int launch_reset(sara_ctx* c) {
 int launch_decide(sara_ctx* c) {
   hipLaunchKernelGGL(k_decide, dim3(1), dim3(kCtlThreads), 0, c->stream, c->ctl, c->cp_dev, c->status,
                      c->n_iss, c->n_done, c->succ, c->infl, c->peff, c->slot_uid, c->slot_j, c->fin,
-                     c->r_len, c->r_reward, c->queue, c->log_dec, c->log_fin);
+                     c->r_len, c->r_reward, c->queue, c->log_dec, c->log_fin, c->prior_a, c->prior_b);
   return SARA_OK;
 }
 
 int launch_refill(sara_ctx* c) {
   hipLaunchKernelGGL(k_refill, dim3(1), dim3(kCtlThreads), 0, c->stream, c->ctl, c->cp_dev, c->status,
                      c->n_iss, c->infl, c->peff, c->slot_uid, c->slot_j, c->slot_gen, c->slot_hash,
-                     c->active, c->queue, c->btab, c->log_draw, c->log_asg);
+                     c->active, c->queue, c->btab, c->log_draw, c->log_asg, c->prior_p);
+  return SARA_OK;
+}
+
+int launch_warm_priors(sara_ctx* c) {
+  hipLaunchKernelGGL(k_warm_priors, dim3((c->U + 255) / 256), dim3(256), 0, c->stream, c->ctl, c->cp_dev,
+                     c->warm_ids, (const double*)c->warm_a, (const double*)c->warm_b, c->warm_n, c->prior_a,
+                     c->prior_b, c->prior_p);
+  return SARA_OK;
+}
+
+int launch_warm_update(sara_ctx* c, double lambda) {
+  hipLaunchKernelGGL(k_warm_add, dim3((c->U + 255) / 256), dim3(256), 0, c->stream, c->ctl, c->warm_ids, c->U,
+                     c->warm_n, c->n_done, c->succ, c->warm_a, c->warm_b);
+  hipLaunchKernelGGL(k_warm_decay, dim3(std::min((c->warm_n + 255) / 256, 1024)), dim3(256), 0, c->stream,
+                     c->warm_a, c->warm_b, c->warm_n, lambda);
   return SARA_OK;
 }
 

@@ -249,6 +249,9 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   ALLOC(c->btab, sizeof(int32_t) * (size_t)(c->S + c->U) * c->MAXB);
   ALLOC(c->rope, sizeof(float2) * (size_t)c->max_pos * (c->hd / 2));
   ALLOC(c->row_rope, sizeof(float2) * (size_t)c->S * (c->hd / 2));
+  ALLOC(c->prior_a, sizeof(double) * (size_t)c->U);
+  ALLOC(c->prior_b, sizeof(double) * (size_t)c->U);
+  ALLOC(c->prior_p, sizeof(double) * (size_t)c->U);
   ALLOC(c->attn_items, sizeof(AttnItem) * (size_t)c->S * c->dec_splits_max);
   ALLOC(c->attn_nitems, sizeof(int32_t) * 4);
   // prompt pool
@@ -418,15 +421,42 @@ extern "C" int sara_begin_step(sara_ctx* c, const int32_t* d_tokens, const int32
   c->step_index = step_index;
   c->cp.step = step_index;
   c->cp.has_flen = c->has_flen;
+  c->cp.has_prior = c->warm_ids ? 1 : 0;
   HIP_TRY(hipMemcpyAsync(c->cp_dev, &c->cp, sizeof(CtlParams), hipMemcpyHostToDevice, st), "params");
   // the host copies above come from pageable memory owned by the context;
   // make sure they have landed before the next step can rewrite them
   HIP_TRY(hipStreamSynchronize(st), "begin_step sync");
   launch_reset(c);
+  if (c->warm_ids) launch_warm_priors(c);
   launch_prefill(c);
   launch_refill(c);
   HIP_TRY(hipGetLastError(), "begin_step launch");
   c->in_step = true;
+  c->warm_step = c->warm_ids != nullptr;
+  return SARA_OK;
+}
+
+extern "C" int sara_set_warm_start(sara_ctx* c, const int32_t* d_ids, double* d_a, double* d_b,
+                                   int32_t n_store) {
+  if (!c) return einval("null context");
+  if (d_ids && (!d_a || !d_b)) return einval("warm start needs d_a and d_b");
+  if (d_ids && n_store < 1) return einval("n_store must be >= 1");
+  c->warm_ids = d_ids;
+  c->warm_a = d_ids ? d_a : nullptr;
+  c->warm_b = d_ids ? d_b : nullptr;
+  c->warm_n = d_ids ? n_store : 0;
+  return SARA_OK;
+}
+
+extern "C" int sara_warm_start_update(sara_ctx* c, double lambda) {
+  if (!c) return einval("null context");
+  if (!(lambda >= 0.0 && lambda <= 1.0)) return einval("lambda must be in [0, 1]");
+  if (!c->warm_ids || !c->warm_step) {
+    set_error("sara_warm_start_update needs a step begun with warm start set");
+    return SARA_ESTATE;
+  }
+  launch_warm_update(c, lambda);
+  HIP_TRY(hipGetLastError(), "warm start update launch");
   return SARA_OK;
 }
 

@@ -73,6 +73,7 @@ struct CtlParams {
   uint32_t forced_eos;
   float temperature;
   int32_t has_flen;
+  int32_t has_prior;             // per-prompt priors (warm start) in place of (a0, b0, prior)
 };
 
 }  // namespace sara
@@ -126,6 +127,13 @@ struct sara_ctx {
   sara::Ctl* ctl = nullptr;
   int32_t *status = nullptr, *n_iss = nullptr, *n_done = nullptr, *succ = nullptr, *infl = nullptr;
   double* peff = nullptr;
+  // history warm start: per-prompt priors of the pool ([U] each) and the
+  // caller's prompt-set state (set by sara_set_warm_start)
+  double *prior_a = nullptr, *prior_b = nullptr, *prior_p = nullptr;
+  const int32_t* warm_ids = nullptr;
+  double *warm_a = nullptr, *warm_b = nullptr;
+  int32_t warm_n = 0;
+  bool warm_step = false;         // the current step began with warm start set
   int32_t *slot_uid = nullptr, *slot_j = nullptr, *slot_gen = nullptr, *fin = nullptr;
   uint64_t* slot_hash = nullptr;
   int32_t* active = nullptr;
@@ -200,6 +208,8 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
 // launchers (controller)
 int launch_reset(sara_ctx* c);
 int launch_decide(sara_ctx* c);
+int launch_warm_priors(sara_ctx* c);
+int launch_warm_update(sara_ctx* c, double lambda);
 int launch_refill(sara_ctx* c);
 int launch_finish(sara_ctx* c, float eps);
 int launch_peff(const int32_t* n, const int32_t* s, int k, double a0, double b0, int count,

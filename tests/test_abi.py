@@ -84,6 +84,8 @@ def test_pure_entry_points_validate_arguments():
     assert L.grpo_group_advantages(None, None, -2, 1e-6, None, None) == sara.SARA_EINVAL
     assert L.grpo_group_advantages(None, None, 3, 1e-6, None, None) == sara.SARA_EINVAL
     assert L.sara_sample_logits(None, 4, 0, None, None, 0, 0, 1.0, -1, 0, None, None) == sara.SARA_EINVAL
+    assert L.sara_set_warm_start(None, None, None, None, 0) == sara.SARA_EINVAL
+    assert L.sara_warm_start_update(None, 0.5) == sara.SARA_EINVAL
     assert L.sara_begin_step(None, None, None, None, None, 0) == sara.SARA_EINVAL
     assert L.sara_decode_step(None, None, None, 0) == sara.SARA_EINVAL
     assert L.sara_posterior_decide(None) == sara.SARA_EINVAL

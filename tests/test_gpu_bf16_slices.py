@@ -162,3 +162,31 @@ def test_bf16_two_layer_truncation_strict(name):
     assert worst_max <= 3e-2
     check_fused_sampler_exact(cfg, gpu, seed, pool["step"])
     ctx.close()
+
+
+def test_bf16_two_layer_long_context_strict():
+    """Prompts of 300-720 tokens (19-45 KV pages) and up to 40 new tokens
+    (private segments over up to 3 pages), 2 layers at full width and
+    vocabulary: every decode row's attention spans several 8-page context
+    splits, so the step's split work list, the multi-split partials and their
+    merge are all checked element-wise against the oracle's logits."""
+    full = W.get_config("qwen1p5b_shape")
+    cfg = W.parity_slice(full, B=2, N=16, prompt_len=(300, 720), max_new=40, pool_U=8)
+    cfg["model"]["n_layers"] = 2
+    w = W.make_weights(cfg)
+    pool = W.make_pool(cfg, 0)
+    plen = np.diff(pool["offsets"])
+    assert plen.min() - 1 > 8 * 16      # more than one split of 8 pages for every row
+    seed = W.sampling_seed(cfg)
+    ora = ORUN.run_step(cfg, w, pool, seed, keep_logits=lambda u, j, i: True)
+    assert max(d["length"] for d in ora["rollouts_detail"].values()) > 16   # a second private page
+    ctx, _ = device_setup(cfg, w)
+    gpu = run_gpu_step(ctx, cfg, pool, forced=forced_table(cfg, ora["rollouts_detail"]), capture_logits=True)
+    compare_logs(gpu["logs"], ora)
+    errs = row_errors(gpu, ora["logits"])
+    worst_max = max(e["max"] for e in errs)
+    print(f"[slice-2L-long] {len(errs)} rows, prompts {plen.min()}-{plen.max()}: max|d|/rms {worst_max:.4f}",
+          flush=True)
+    assert worst_max <= 3e-2
+    check_fused_sampler_exact(cfg, gpu, seed, pool["step"])
+    ctx.close()

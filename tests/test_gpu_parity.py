@@ -237,3 +237,62 @@ def test_saturated_pool_abandoned_after_probe(torch_cuda):
     assert np.all(ro["status"][:drawn] == 3) and np.all(ro["n"][:drawn] == 4)
     assert gpu["stats"]["rollouts"] == 4 * drawn
     ctx.close()
+
+
+@pytest.mark.parametrize("lam", [0.5, 1.0])
+def test_warm_start_multi_step_model_free(torch_cuda, lam):
+    """History warm start over a revisited prompt set: four allocation steps
+    with the 1.5B workload's allocation (B=64, k=8, N=512, 512 slots), each
+    pool 256 distinct prompts of a 512-prompt set, tokens from a table
+    (decoder skipped).  Every step's decision / draw / assignment / finish
+    logs are bit-exact against the oracle run under the oracle's carried
+    priors, and after every step the device pseudo-counts equal the oracle's
+    update exactly."""
+    from oracle import warm as OW
+    torch = torch_cuda
+    full = W.get_config("qwen1p5b_shape")
+    cfg = W.get_config("tiny_f32")
+    cfg["alloc"] = dict(full["alloc"])
+    cfg["alloc"]["max_prompt"] = 32
+    cfg["alloc"]["max_new"] = 64
+    cfg["model"]["eos_id"] = 511
+    cfg["index"] = full["index"]
+    cfg["prompt_len"] = (8, 32)
+    a = cfg["alloc"]
+    U = a["pool_U"]
+    D = 2 * U
+    pset = W.prompt_set(cfg, D)
+    w = W.make_weights(W.get_config("tiny_f32"))
+    ctx, _ = device_setup(cfg, w)
+    seed = W.sampling_seed(cfg)
+    ca, cb = [0.0] * D, [0.0] * D
+    d_a = torch.zeros(D, dtype=torch.float64, device="cuda")
+    d_b = torch.zeros(D, dtype=torch.float64, device="cuda")
+    saved = []
+    for step in range(4):
+        pool = W.set_pool(cfg, pset, step)
+        assert len(set(pool["ids"].tolist())) == U
+        d_ids = torch.from_numpy(pool["ids"]).cuda()
+        ctx.sara_set_warm_start(d_ids, d_a, d_b)
+        tab = _model_free_case(cfg, 30 + step)
+        g = np.random.default_rng(40 + step)
+        tab[g.random(tab.shape) < 1 / 20] = 511
+        print(f"[warm] lambda {lam} step {step}", flush=True)
+        gpu = run_gpu_step(ctx, cfg, pool, forced=tab, model_free=True)
+        ctx.sara_warm_start_update(lam)
+        pri = OW.priors(pool["ids"], ca, cb, a["alpha0"], a["beta0"])
+        ora = ORUN.run_step(cfg, None, pool, seed, forced_tokens=tab, model_free=True, priors=pri)
+        compare_logs(gpu["logs"], ora)
+        st = gpu["stats"]
+        assert (st["committed"], st["rollouts"], st["tokens"], st["decode_steps"], st["budget_left"]) == (
+            ora["n_committed"], ora["rollouts"], ora["tokens"], ora["decode_steps"], ora["budget_left"])
+        assert st["error"] == 0
+        ca, cb = OW.update(ca, cb, pool["ids"].tolist(), ora["n_done"], ora["successes"], ora["drawn"], lam)
+        torch.cuda.synchronize()
+        assert np.array_equal(d_a.cpu().numpy(), np.array(ca))
+        assert np.array_equal(d_b.cpu().numpy(), np.array(cb))
+        saved.append(ora["rollouts"] / max(ora["drawn"], 1))
+        del d_ids
+    ctx.sara_set_warm_start(None)
+    print(f"[warm] rollouts per drawn prompt by step: {[round(x, 3) for x in saved]}", flush=True)
+    ctx.close()

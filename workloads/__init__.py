@@ -238,6 +238,52 @@ def make_pool(cfg: dict, step: int = 0) -> dict:
     return dict(tokens=tokens, offsets=offsets, p=p, forced_len=forced, step=step)
 
 
+def prompt_set(cfg: dict, D: int) -> dict:
+    """A finite set of D prompts revisited across allocation steps (history
+    warm start): tokens (concatenated), offsets (D+1) and success rates p,
+    drawn like a pool's (lengths U[prompt_len], tokens uniform in [0, V-1),
+    p from the workload's step-0 mixture)."""
+    m = cfg["model"]
+    master = master_seed(cfg)
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([master, 4, D])))
+    lo, hi = cfg["prompt_len"]
+    lens = np.minimum(g.integers(lo, hi + 1, size=D), cfg["alloc"]["max_prompt"]).astype(np.int32)
+    offsets = np.zeros(D + 1, dtype=np.int32)
+    offsets[1:] = np.cumsum(lens)
+    tokens = g.integers(0, m["vocab"] - 1, size=int(offsets[-1])).astype(np.int32)
+    wh, we, wm = mixture_weights(cfg, 0)
+    comp = g.choice(3, size=D, p=[wh, we, wm])
+    p = np.where(comp == 0, g.beta(0.3, 3.0, size=D),
+                 np.where(comp == 1, g.beta(3.0, 0.3, size=D), g.random(size=D))).astype(np.float64)
+    return dict(tokens=tokens, offsets=offsets, p=p)
+
+
+def set_pool(cfg: dict, pset: dict, step: int) -> dict:
+    """Pool of one allocation step over a prompt set: pool_U distinct set
+    prompts chosen per step (seeded), in that order; `ids` maps pool index
+    to set index.  Forced lengths (if the workload has them) as make_pool's."""
+    a = cfg["alloc"]
+    U, k = a["pool_U"], a["k"]
+    D = len(pset["p"])
+    master = master_seed(cfg)
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([master, 5, step])))
+    ids = g.choice(D, size=U, replace=False).astype(np.int32)
+    offs = pset["offsets"]
+    parts = [pset["tokens"][offs[i]:offs[i + 1]] for i in ids]
+    lens = np.array([len(x) for x in parts], dtype=np.int32)
+    offsets = np.zeros(U + 1, dtype=np.int32)
+    offsets[1:] = np.cumsum(lens)
+    forced = None
+    fl = cfg.get("forced_len")
+    if fl is not None:
+        h = np.random.Generator(np.random.PCG64(np.random.SeedSequence([master, 2, step])))
+        z = h.standard_normal(size=(U, k))
+        L = np.rint(np.exp(fl["mu"] + fl["sigma"] * z))
+        forced = np.clip(L, 1, min(fl["cap"], a["max_new"])).astype(np.int32)
+    return dict(tokens=np.concatenate(parts).astype(np.int32), offsets=offsets,
+                p=pset["p"][ids].astype(np.float64), forced_len=forced, step=step, ids=ids)
+
+
 def saturated_pool(pool: dict, seed: int = 7) -> dict:
     """Same prompts with every success rate forced to 0 or 1."""
     q = dict(pool)
