@@ -41,7 +41,19 @@ enum {
   SARA_EDEVICE = -5   /* a device-side check failed (see sara_step_stats.error) */
 };
 enum { SARA_F32 = 0, SARA_BF16 = 1 };
-enum { SARA_MODE_SARA = 0, SARA_MODE_FIXED_K = 1 };
+/* SARA_MODE_SARA_THOMPSON: SARA with the posterior-sampling priority of the
+ * index-policy proposition (Thompson sampling as the alternative index to
+ * p_eff): when a prompt's rollouts are queued (at its draw, or at a CONTINUE
+ * decision after n outcomes with s successes) it draws g ~ Beta(a, b), its
+ * current posterior (a = alpha0 + s, b = beta0 + n - s), as the a-th
+ * smallest of a + b - 1 uniforms (w + 1/2) 2^-32, w the words of
+ * Philox4x32-10 under the sampler's key at counters (uid, n, c, 2), and its
+ * pending rollouts are ordered by P(group of k ends mixed | g) (Eq. peff at
+ * the draw: 1 - g^k - (1-g)^k, 1 - (1-g)^r after s = 0, 1 - g^r after
+ * s = n, r = k - n; powers by repeated fp64 multiplication) instead of
+ * p_eff.  Decisions are unchanged.  A prompt whose posterior parameters are
+ * not integers, or with a + b - 1 > 4096, keeps the p_eff index. */
+enum { SARA_MODE_SARA = 0, SARA_MODE_FIXED_K = 1, SARA_MODE_SARA_THOMPSON = 2 };
 /* decision codes in the decision log */
 enum { SARA_COMMIT = 1, SARA_ABANDON = 2, SARA_CONTINUE = 3 };
 /* per-prompt status */
@@ -64,6 +76,7 @@ typedef struct {
 
 /* Allocation problem of one step (Algorithm 1 inputs; implementation-details
  * appendix for commit_min, the prior and the budget cap):
+ *   mode        SARA_MODE_SARA, SARA_MODE_FIXED_K or SARA_MODE_SARA_THOMPSON
  *   B           effective groups wanted (ignored in SARA_MODE_FIXED_K)
  *   k           group size;  n0 probe rollouts per fresh prompt (1..k)
  *   commit_min  commit floor (2..k); tau_low abandon threshold in [0, 1]

@@ -35,15 +35,21 @@ History warm start (implementation details, "defaults and history
 warm-start"): `priors` gives each pool prompt its own Beta(alpha0_u,
 beta0_u) prior (see warm.py); its p_eff, decisions and the priority of its
 probes then use that prior in place of Beta(alpha0, beta0).
+
+mode "sara_thompson": pending rollouts are ordered by the posterior-sampling
+index of thompson.py (drawn when they are queued, keyed by draw_key = (seed,
+step index)) instead of p_eff; everything else is unchanged.
 """
+from . import thompson
 from .predictor import ABANDON, COMMIT, CONTINUE, decide, p_eff, priority_key
 
 UNDRAWN, ACTIVE, COMMITTED, ABANDONED = 0, 1, 2, 3
 
 
-def simulate(alloc: dict, U: int, outcomes, priors=None):
+def simulate(alloc: dict, U: int, outcomes, priors=None, draw_key=(0, 0)):
     """outcomes(list[(uid, j)]) -> list[(length, reward)] for newly started rollouts.
     priors: optional (alpha0_u, beta0_u) sequences of length U (warm start).
+    draw_key: (seed, step index) of the posterior-sampling priority.
 
     Returns a dict with the decision / draw / assignment / finish logs and the
     per-prompt and per-rollout results."""
@@ -51,6 +57,7 @@ def simulate(alloc: dict, U: int, outcomes, priors=None):
     tau, a0, b0 = alloc["tau_low"], alloc["alpha0"], alloc["beta0"]
     N, S, bits = alloc["budget_N"], alloc["n_slots"], alloc["prio_quant_bits"]
     fixed_k = alloc["mode"] == "fixed_k"
+    ts = alloc["mode"] == "sara_thompson"
 
     status = [UNDRAWN] * U
     n_iss, n_done, succ, infl = [0] * U, [0] * U, [0] * U, [0] * U
@@ -66,6 +73,10 @@ def simulate(alloc: dict, U: int, outcomes, priors=None):
         pa, pb = [float(x) for x in priors[0]], [float(x) for x in priors[1]]
         assert len(pa) == U and len(pb) == U
     prior = [p_eff(0, 0, k, pa[u], pb[u]) for u in range(U)]
+    prio = [0.0] * U        # index of the prompt's pending rollouts
+
+    def queue_index(u, n, s, pv):
+        return thompson.index(draw_key[0], draw_key[1], u, n, s, k, pa[u], pb[u]) if ts else pv
 
     def refill(start):
         nonlocal budget, next_uid, nA
@@ -76,11 +87,12 @@ def simulate(alloc: dict, U: int, outcomes, priors=None):
             budget -= k
             nA += 1
             pe[u] = prior[u]
+            prio[u] = queue_index(u, 0, 0, prior[u])
             n_iss[u] = n0
             infl[u] = n0
             Q.extend((u, j) for j in range(n0))
             log_draw.append((start, u))
-        Q.sort(key=lambda e: (-priority_key(pe[e[0]], bits), e[0], e[1]))
+        Q.sort(key=lambda e: (-priority_key(prio[e[0]], bits), e[0], e[1]))
         free = [i for i in range(S) if slots[i] is None]
         m = min(len(free), len(Q))
         started = Q[:m]
@@ -125,6 +137,7 @@ def simulate(alloc: dict, U: int, outcomes, priors=None):
                 nA -= 1
                 budget += k - n
             else:
+                prio[u] = queue_index(u, n, s, pv)
                 Q.extend((u, n_iss[u] + i) for i in range(more))
                 n_iss[u] += more
                 infl[u] += more

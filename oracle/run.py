@@ -124,7 +124,8 @@ def run_step(cfg, weights, pool, seed, forced_tokens=None, keep_logits=None, mod
     """priors: optional per pool prompt (alpha0_u, beta0_u) (history warm start)."""
     src = RolloutSource(cfg, weights, pool, seed, forced_tokens=forced_tokens,
                         keep_logits=keep_logits, model_free=model_free, gemm_acc=gemm_acc)
-    res = controller.simulate(cfg["alloc"], len(pool["p"]), src.outcomes, priors=priors)
+    res = controller.simulate(cfg["alloc"], len(pool["p"]), src.outcomes, priors=priors,
+                              draw_key=(seed, pool["step"]))
     k = cfg["alloc"]["k"]
     offs, rws = [0], []
     for u in res["committed"]:

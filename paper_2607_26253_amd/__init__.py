@@ -17,7 +17,8 @@ LIB_PATH = os.path.join(_HERE, "libsara.so")
 
 SARA_OK, SARA_EINVAL, SARA_ENOMEM, SARA_EHIP, SARA_ESTATE, SARA_EDEVICE = 0, -1, -2, -3, -4, -5
 SARA_F32, SARA_BF16 = 0, 1
-SARA_MODE_SARA, SARA_MODE_FIXED_K = 0, 1
+SARA_MODE_SARA, SARA_MODE_FIXED_K, SARA_MODE_SARA_THOMPSON = 0, 1, 2
+_MODES = {"sara": SARA_MODE_SARA, "fixed_k": SARA_MODE_FIXED_K, "sara_thompson": SARA_MODE_SARA_THOMPSON}
 SARA_COMMIT, SARA_ABANDON, SARA_CONTINUE = 1, 2, 3
 
 EXPORTED = ["sara_init", "sara_begin_step", "sara_decode_step", "sara_posterior_decide",
@@ -143,7 +144,7 @@ def alloc_desc(alloc: dict, seed: int) -> sara_alloc_desc:
         alloc["B"], alloc["k"], alloc["n0"], alloc["commit_min"], float(alloc["tau_low"]),
         float(alloc["alpha0"]), float(alloc["beta0"]), int(alloc["budget_N"]), alloc["pool_U"],
         alloc["n_slots"], alloc["kv_block"], alloc["max_prompt"], alloc["max_new"],
-        SARA_MODE_FIXED_K if alloc["mode"] == "fixed_k" else SARA_MODE_SARA,
+        _MODES[alloc["mode"]],
         float(alloc["temperature"]), float(alloc["top_p"]), int(alloc["forced_eos_u32"]),
         alloc["prio_quant_bits"], int(seed) & ((1 << 64) - 1))
 

@@ -35,6 +35,48 @@ __device__ __forceinline__ uint64_t queue_key(double pe, int bits, int uid, int 
   return (inv << 42) | ((uint64_t)uid << 16) | (uint64_t)j;
 }
 
+// Posterior-sampling priority index (SARA_MODE_SARA_THOMPSON): P(the group
+// of k ends mixed | g) at one draw g ~ Beta(a, b) of the posterior a = a0 + s,
+// b = b0 + n - s.  For integer a, b the draw is the a-th smallest of
+// m = a + b - 1 uniforms (w + 1/2) 2^-32, w the words of Philox4x32-10 at
+// counters (uid, n, c, 2) under the sampler key: found as the smallest word
+// value v with #{w_i <= v} >= a by bisection over the 32-bit range,
+// regenerating the m words per probe (no per-thread storage).  Other
+// posteriors keep p_eff.
+constexpr int kThompsonMaxM = 4096;
+__device__ double pow_seq(double x, int e) {
+  double p = 1.0;
+  for (int i = 0; i < e; ++i) p = p * x;
+  return p;
+}
+__device__ double thompson_index(const CtlParams& cp, int uid, int n, int s, double a0, double b0) {
+  if (s >= 1 && n - s >= 1) return 1.0;
+  const int r = cp.k - n;
+  if (r <= 0) return 0.0;
+  const double a = a0 + (double)s, b = b0 + (double)(n - s);
+  if (a != floor(a) || b != floor(b) || a < 1.0 || b < 1.0 || a + b - 1.0 > (double)kThompsonMaxM)
+    return peff_dev(n, s, cp.k, a0, b0);
+  const int ia = (int)a, m = (int)(a + b) - 1;
+  uint32_t k0, k1;
+  sampler_key(cp.seed, cp.step, k0, k1);
+  uint32_t lo = 0u, hi = 0xFFFFFFFFu;
+  while (lo < hi) {
+    const uint32_t mid = lo + ((hi - lo) >> 1);
+    int cnt = 0;
+    for (int c = 0; 4 * c < m; ++c) {
+      const U32x4 w = philox4x32_10((uint32_t)uid, (uint32_t)n, (uint32_t)c, 2u, k0, k1);
+      const int e = m - 4 * c;   // words of this counter that are draws
+      cnt += (w.x <= mid) + (e > 1 && w.y <= mid) + (e > 2 && w.z <= mid) + (e > 3 && w.w <= mid);
+    }
+    if (cnt >= ia) hi = mid;
+    else lo = mid + 1u;
+  }
+  const double g = ((double)lo + 0.5) * 0x1p-32;
+  if (n == 0) return (1.0 - pow_seq(g, cp.k)) - pow_seq(1.0 - g, cp.k);
+  if (s == 0) return 1.0 - pow_seq(1.0 - g, r);
+  return 1.0 - pow_seq(g, r);
+}
+
 // ---------------------------------------------------------------------------
 // reset (start of an allocation step)
 // ---------------------------------------------------------------------------
@@ -163,8 +205,11 @@ __global__ __launch_bounds__(kCtlThreads) void k_decide(Ctl* __restrict__ ctl, c
         atomicAdd(&s_refund, (unsigned long long)(cp.k - n));
       } else {
         int j0 = n_iss[u];
+        const double qi = (cp.mode == SARA_MODE_SARA_THOMPSON)
+            ? thompson_index(cp, u, n, s, cp.has_prior ? prior_a[u] : cp.a0, cp.has_prior ? prior_b[u] : cp.b0)
+            : pe;
         for (int e = 0; e < more; ++e)
-          queue[s_qlen + exm + e] = queue_key(pe, cp.bits, u, j0 + e);
+          queue[s_qlen + exm + e] = queue_key(qi, cp.bits, u, j0 + e);
         n_iss[u] = j0 + more;
         infl[u] = more;  // it was 0: the prompt was quiescent
       }
@@ -195,7 +240,8 @@ __global__ __launch_bounds__(kCtlThreads) void k_refill(Ctl* __restrict__ ctl, c
     double* __restrict__ peff, int32_t* __restrict__ slot_uid, int32_t* __restrict__ slot_j,
     int32_t* __restrict__ slot_gen, uint64_t* __restrict__ slot_hash,
     int32_t* __restrict__ active, uint64_t* __restrict__ queue, int32_t* __restrict__ btab,
-    int64_t* __restrict__ log_draw, int64_t* __restrict__ log_asg, const double* __restrict__ prior_p) {
+    int64_t* __restrict__ log_draw, int64_t* __restrict__ log_asg, const double* __restrict__ prior_p,
+    const double* __restrict__ prior_a, const double* __restrict__ prior_b) {
   __shared__ int buf[kCtlThreads];
   __shared__ uint64_t qs[kMaxQueue];
   __shared__ int freel[kMaxSlots];
@@ -218,7 +264,7 @@ __global__ __launch_bounds__(kCtlThreads) void k_refill(Ctl* __restrict__ ctl, c
     int64_t d = (int64_t)cp.U - ctl->next_uid;
     int64_t byb = bud / cp.k;
     if (byb < d) d = byb;
-    if (cp.mode == SARA_MODE_SARA) {
+    if (cp.mode != SARA_MODE_FIXED_K) {
       int64_t need = (int64_t)cp.B - ctl->nC - ctl->nA;
       if (need < d) d = need;
     }
@@ -251,7 +297,10 @@ __global__ __launch_bounds__(kCtlThreads) void k_refill(Ctl* __restrict__ ctl, c
     else if (e < qlen) {
       int q = e - s_qlen;
       const int uq = nu0 + q / cp.n0;
-      key = queue_key(cp.has_prior ? prior_p[uq] : cp.prior, cp.bits, uq, q % cp.n0);
+      const double qi = (cp.mode == SARA_MODE_SARA_THOMPSON)
+          ? thompson_index(cp, uq, 0, 0, cp.has_prior ? prior_a[uq] : cp.a0, cp.has_prior ? prior_b[uq] : cp.b0)
+          : (cp.has_prior ? prior_p[uq] : cp.prior);
+      key = queue_key(qi, cp.bits, uq, q % cp.n0);
     }
     qs[e] = key;
   }
@@ -470,7 +519,7 @@ int launch_decide(sara_ctx* c) {
 int launch_refill(sara_ctx* c) {
   hipLaunchKernelGGL(k_refill, dim3(1), dim3(kCtlThreads), 0, c->stream, c->ctl, c->cp_dev, c->status,
                      c->n_iss, c->infl, c->peff, c->slot_uid, c->slot_j, c->slot_gen, c->slot_hash,
-                     c->active, c->queue, c->btab, c->log_draw, c->log_asg, c->prior_p);
+                     c->active, c->queue, c->btab, c->log_draw, c->log_asg, c->prior_p, c->prior_a, c->prior_b);
   return SARA_OK;
 }
 

@@ -174,7 +174,8 @@ static int validate(const sara_model_desc* m, const sara_alloc_desc* a) {
   if (a->n_slots < 1 || a->n_slots > kMaxSlots) return einval("n_slots must be in [1, 4096]");
   if (a->kv_block != kBlockTok) return einval("kv_block must be 16");
   if (a->max_prompt < 1 || a->max_new < 1) return einval("max_prompt and max_new must be >= 1");
-  if (a->mode != SARA_MODE_SARA && a->mode != SARA_MODE_FIXED_K) return einval("unknown mode");
+  if (a->mode != SARA_MODE_SARA && a->mode != SARA_MODE_FIXED_K && a->mode != SARA_MODE_SARA_THOMPSON)
+    return einval("unknown mode");
   if (!(a->temperature > 0.f)) return einval("temperature must be > 0");
   if (a->top_p != 1.0f) return einval("top_p must be 1 (nucleus truncation is not implemented)");
   if (a->prio_quant_bits < 1 || a->prio_quant_bits > 21) return einval("prio_quant_bits must be in [1, 21]");

@@ -174,19 +174,25 @@ def _model_free_case(cfg, U_tokens_seed=3):
 @pytest.mark.parametrize("name,mode", [("qwen1p5b_shape", "sara"), ("long_ragged_1p5b", "sara"),
                                        ("pool_3b", "sara"), ("pool_3b", "fixed_k"),
                                        ("qwen3b_shape", "sara"),
-                                       ("qwen1p5b_shape", "commit_min=2"), ("qwen1p5b_shape", "commit_min=4")])
+                                       ("qwen1p5b_shape", "commit_min=2"), ("qwen1p5b_shape", "commit_min=4"),
+                                       ("long_ragged_1p5b", "sara_thompson")])
 def test_controller_full_size_model_free(torch_cuda, name, mode):
     """Full-size allocation parameters of each workload; tokens from a table
     (decoder skipped), so the controller, hash reward and termination are
     checked bit-exactly against the oracle's event simulation.  The
     commit_min cases are the early-commit variant (commit at the first mix,
     Theorem 2's proof, and the floor of 4 of the commit-floor ablation): groups
-    of 2..8 rollouts, so the GRPO advantages run over variable group sizes."""
+    of 2..8 rollouts, so the GRPO advantages run over variable group sizes.
+    The sara_thompson case orders pending rollouts by the posterior-sampling
+    index on the workload whose 256 slots bind, so its assignment log differs
+    from the p_eff ordering's and must still match the oracle exactly."""
     full = W.get_config(name)
     if mode == "fixed_k":
         full = W.fixed_k_variant(full)
     elif mode.startswith("commit_min="):
         full["alloc"]["commit_min"] = int(mode.split("=")[1])
+    elif mode == "sara_thompson":
+        full["alloc"]["mode"] = "sara_thompson"
     cfg = W.get_config("tiny_f32")
     cfg["alloc"] = dict(full["alloc"])
     cfg["alloc"]["max_prompt"] = 32
@@ -220,6 +226,10 @@ def test_controller_full_size_model_free(torch_cuda, name, mode):
     if mode.startswith("commit_min="):
         sizes = np.diff(off)
         assert sizes.size == 0 or sizes.min() >= a["commit_min"]
+    if mode == "sara_thompson":
+        ref = ORUN.run_step(dict(cfg, alloc=dict(a, mode="sara")), None, pool, seed, forced_tokens=tab,
+                            model_free=True)
+        assert ref["log_assign"] != ora["log_assign"], "slots never bound: the priority made no difference"
     ctx.close()
 
 
