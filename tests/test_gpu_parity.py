@@ -306,3 +306,83 @@ def test_warm_start_multi_step_model_free(torch_cuda, lam):
     ctx.sara_set_warm_start(None)
     print(f"[warm] rollouts per drawn prompt by step: {[round(x, 3) for x in saved]}", flush=True)
     ctx.close()
+
+
+def _edge_pool(cfg, lengths):
+    """The workload's pool with prompt lengths cycled from `lengths` (tokens
+    regenerated, uniform in [0, V-1))."""
+    pool = W.make_pool(cfg, 0)
+    U = len(pool["p"])
+    lens = np.array([lengths[u % len(lengths)] for u in range(U)], dtype=np.int32)
+    offsets = np.zeros(U + 1, dtype=np.int32)
+    offsets[1:] = np.cumsum(lens)
+    g = np.random.default_rng(77)
+    pool["tokens"] = g.integers(0, cfg["model"]["vocab"] - 1, size=int(offsets[-1])).astype(np.int32)
+    pool["offsets"] = offsets
+    return pool
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "qwen1p5b_shape"])
+def test_prompt_length_edges(torch_cuda, name):
+    """Prompts of 1 token (no prompt KV: the first generated token attends to
+    itself only), 2, 15-17 (one page and its neighbours), 31-33 and the
+    maximum; teacher-forced logits against the oracle (fp32: <= 1e-3; bf16
+    2-layer slice: <= 3e-2 rms) and every log bit-exact."""
+    from tests.test_gpu_bf16_slices import row_errors
+    if name == "tiny_f32":
+        cfg = W.get_config("tiny_f32")
+        cfg["alloc"].update(B=4, budget_N=32, n_slots=32, pool_U=16, max_new=12)
+        lengths = [1, 16, 17, 32, 2, 15, 31, 1]
+    else:
+        full = W.get_config(name)
+        cfg = W.parity_slice(full, B=3, N=32, prompt_len=(1, 48), max_new=10, pool_U=8)
+        cfg["model"]["n_layers"] = 2
+        lengths = [1, 17, 16, 48, 2, 15, 33, 1]
+    w = W.make_weights(cfg)
+    pool = _edge_pool(cfg, lengths)
+    seed = W.sampling_seed(cfg)
+    ora = ORUN.run_step(cfg, w, pool, seed, keep_logits=lambda u, j, i: True)
+    drawn_lens = {int(pool["offsets"][u + 1] - pool["offsets"][u]) for (u, _j) in ora["rollouts_detail"]}
+    assert 1 in drawn_lens and 16 in drawn_lens and 17 in drawn_lens
+    ctx, _ = device_setup(cfg, w)
+    gpu = run_gpu_step(ctx, cfg, pool, forced=forced_table(cfg, ora["rollouts_detail"]), capture_logits=True)
+    compare_logs(gpu["logs"], ora)
+    if name == "tiny_f32":
+        worst = max(float(np.max(np.abs(gpu["logits"][t][s] - ora["logits"][(u, j, i)])))
+                    for (t, s), (u, j, i) in slot_rows(gpu).items())
+        assert worst <= 1e-3, worst
+    else:
+        worst = max(e["max"] for e in row_errors(gpu, ora["logits"]))
+        assert worst <= 3e-2, worst
+    print(f"[edges] {name}: prompt lengths {sorted(drawn_lens)}, worst {worst:.3g}", flush=True)
+    ctx.close()
+
+
+@pytest.mark.parametrize("over", [dict(budget_N=7), dict(n_slots=1, budget_N=24), dict(max_new=1),
+                                  dict(n0=8, commit_min=8), dict(n0=1, commit_min=2, B=1),
+                                  dict(pool_U=1, B=4)])
+def test_tiny_allocation_edges(torch_cuda, over):
+    """Degenerate allocations on the fp32 model: a budget below one
+    reservation (nothing drawn, the step ends at once), a single slot, one
+    generated token per rollout, all k probes at once, a goal of one group
+    committed at the first mix, and a one-prompt pool; every log and count
+    bit-exact against the oracle."""
+    cfg = W.get_config("tiny_f32")
+    cfg["alloc"].update(B=4, budget_N=32, n_slots=16, pool_U=12, max_new=6)
+    cfg["alloc"].update(over)
+    w = W.make_weights(cfg)
+    pool = W.make_pool(cfg, 0)
+    seed = W.sampling_seed(cfg)
+    ora = ORUN.run_step(cfg, w, pool, seed, keep_logits=lambda u, j, i: True)
+    ctx, _ = device_setup(cfg, w)
+    gpu = run_gpu_step(ctx, cfg, pool, forced=forced_table(cfg, ora["rollouts_detail"]))
+    compare_logs(gpu["logs"], ora)
+    st = gpu["stats"]
+    assert (st["committed"], st["rollouts"], st["tokens"], st["decode_steps"], st["budget_left"], st["drawn"]) == (
+        ora["n_committed"], ora["rollouts"], ora["tokens"], ora["decode_steps"], ora["budget_left"], ora["drawn"])
+    if over.get("budget_N") == 7:
+        assert st["drawn"] == 0 and st["decode_steps"] == 0 and st["done"] == 1
+    off, r, a = gpu["adv"]
+    assert np.array_equal(off, ora["grpo_offsets"])
+    assert np.allclose(a, ora["advantages"], rtol=1e-6, atol=1e-6)
+    ctx.close()
