@@ -190,3 +190,48 @@ def test_bf16_two_layer_long_context_strict():
     assert worst_max <= 3e-2
     check_fused_sampler_exact(cfg, gpu, seed, pool["step"])
     ctx.close()
+
+
+def test_logical_rollout_keys_give_exact_counterfactuals():
+    """Sampling keyed by the logical rollout id (uid k + j) and the generated
+    index, never by the slot or the batch, makes SARA's first n rollouts of a
+    prompt token-for-token the fixed-k baseline's (full 28-layer 1.5B model,
+    short rollouts).  The fixed-k run then labels every prompt SARA decided
+    with its full group of k: every commit is a mixed group (mixing is
+    absorbing), and the abandoned prompts whose group would have mixed are
+    the counterfactual loss the paper measures against dynamic sampling."""
+    cfg = W.parity_slice(W.get_config("qwen1p5b_shape"), B=8, N=96, max_new=10, pool_U=32)
+    fk = W.fixed_k_variant(cfg)
+    fk["alloc"]["budget_N"] = cfg["alloc"]["pool_U"] * cfg["alloc"]["k"]
+    w = W.make_weights(cfg)
+    pool = W.make_pool(cfg, 0)
+    k = cfg["alloc"]["k"]
+    ctx, _ = device_setup(cfg, w)
+    sara = run_gpu_step(ctx, cfg, pool)
+    ctx.close()
+    ctx, _ = device_setup(fk, w)
+    full = run_gpu_step(ctx, fk, pool)
+    ctx.close()
+    rs, rf = sara["roll"], full["roll"]
+    drawn = sara["stats"]["drawn"]
+    assert full["stats"]["drawn"] >= drawn
+    lost = committed = abandoned = 0
+    for u in range(drawn):
+        n = int(rs["n"][u])
+        for j in range(n):
+            r = u * k + j
+            L = int(rs["length"][r])
+            assert L == int(rf["length"][r]) and L > 0
+            assert np.array_equal(rs["tokens"][r][:L], rf["tokens"][r][:L]), (u, j)
+            assert rs["reward"][r] == rf["reward"][r]
+        s_full = int(sum(rf["reward"][u * k + j] for j in range(k)))
+        mixed_full = 1 <= s_full <= k - 1
+        if rs["status"][u] == 2:
+            committed += 1
+            assert mixed_full
+        elif rs["status"][u] == 3:
+            abandoned += 1
+            lost += int(mixed_full)
+    print(f"[counterfactual] drawn {drawn}: committed {committed}, abandoned {abandoned}, "
+          f"lost (would have mixed) {lost}", flush=True)
+    assert committed + abandoned == drawn and drawn >= 8
