@@ -388,64 +388,69 @@ def test_tiny_allocation_edges(torch_cuda, over):
     ctx.close()
 
 
-def test_tau_sweep_with_exact_counterfactuals(torch_cuda):
-    """The tau ablation on the device, with exact counterfactual labels
-    (section 8(f): abandonment threshold sweep, lost groups, decision
-    quality).  Model-free rollouts of equal length over a 2048-prompt pool of
-    the success-rate mixture; for every tau the fixed-k run on the same
-    table labels each drawn prompt with its full group of k (its first n
-    rewards are SARA's, by the logical rollout keys).  Checked: every
-    abandonment happens at n_a = k - floor(tau (k+1)) on an all-same prefix,
-    every commit at n = k on a mixed one, and the rollouts per drawn prompt
-    match sum_u [n_a + (k - n_a)(1 - p_u^n_a - (1-p_u)^n_a)] within 5 sigma."""
+def test_ablation_sweeps_with_exact_counterfactuals(torch_cuda):
+    """The tau, n0 and k ablations on the device, with exact counterfactual
+    labels (section 8(f): sweeps, lost groups, decision quality).
+    Model-free rollouts of equal length over a 2048-prompt pool of the
+    success-rate mixture; for every k the fixed-k run on the same token table
+    labels each drawn prompt with its full group (its first n rewards are
+    SARA's, by the logical rollout keys).  Checked at every point: each
+    abandonment happens at n_stop = max(n0, k - floor(tau (k+1))) on an
+    all-same prefix, each commit at n = k on a mixed one, and the rollouts
+    per drawn prompt match sum_u [n_stop + (k - n_stop) q_u],
+    q_u = 1 - p_u^n_stop - (1-p_u)^n_stop, within 5 sigma."""
     full = W.get_config("tiny_f32")
-    cfg = W.get_config("tiny_f32")
-    cfg["alloc"].update(B=10 ** 6, budget_N=2048, pool_U=2048, n_slots=512, max_new=4)
-    cfg["model"]["eos_id"] = -1
-    k = cfg["alloc"]["k"]
-    pool = W.make_pool(cfg, 0)
-    p = pool["p"]
-    tab = _model_free_case(cfg, 5)
+    base = W.get_config("tiny_f32")
+    base["alloc"].update(B=10 ** 6, budget_N=2048, pool_U=2048, n_slots=512, max_new=4)
+    base["model"]["eos_id"] = -1
     w = W.make_weights(full)
-    fk = W.fixed_k_variant(cfg)
-    fk["alloc"]["budget_N"] = 4096
-    ctx, _ = device_setup(fk, w)
-    lab = run_gpu_step(ctx, fk, pool, forced=tab, model_free=True)
-    ctx.close()
-    rf = lab["roll"]
-    rows = []
-    for tau in (0.1, 0.3, 0.45, 0.6):
-        c = dict(cfg, alloc=dict(cfg["alloc"], tau_low=tau))
-        ctx, _ = device_setup(c, w)
-        g = run_gpu_step(ctx, c, pool, forced=tab, model_free=True)
+    labels = {}
+
+    def point(k, n0, tau):
+        cfg = dict(base, alloc=dict(base["alloc"], k=k, n0=n0, commit_min=k, tau_low=tau))
+        pool = W.make_pool(cfg, 0)
+        p = pool["p"]
+        tab = _model_free_case(cfg, 5)
+        if k not in labels:
+            fk = W.fixed_k_variant(cfg)
+            fk["alloc"]["budget_N"] = 4096
+            ctx, _ = device_setup(fk, w)
+            labels[k] = run_gpu_step(ctx, fk, pool, forced=tab, model_free=True)
+            ctx.close()
+        lab = labels[k]
+        rf = lab["roll"]
+        ctx, _ = device_setup(cfg, w)
+        g = run_gpu_step(ctx, cfg, pool, forced=tab, model_free=True)
         ctx.close()
         rs, st = g["roll"], g["stats"]
         drawn = st["drawn"]
         assert lab["stats"]["drawn"] >= drawn
-        n_a = min(k, k - math.floor(tau * (k + 1)))
-        lost = 0
-        want = 0.0
-        var = 0.0
+        n_stop = max(n0, min(k, k - math.floor(tau * (k + 1))))
+        lost, want, var = 0, 0.0, 0.0
         for u in range(drawn):
             n, s = int(rs["n"][u]), int(rs["s"][u])
             assert np.array_equal(rs["reward"][u * k:u * k + n], rf["reward"][u * k:u * k + n])
             s_full = int(np.sum(rf["reward"][u * k:(u + 1) * k]))
-            mixed_full = 1 <= s_full <= k - 1
             if rs["status"][u] == 2:
                 assert n == k and 1 <= s <= k - 1
             else:
-                assert rs["status"][u] == 3 and n == n_a and s in (0, n)
-                lost += int(mixed_full)
-            q = 1 - p[u] ** n_a - (1 - p[u]) ** n_a
-            want += n_a + (k - n_a) * q
-            var += (k - n_a) ** 2 * q * (1 - q)
+                assert rs["status"][u] == 3 and n == n_stop and s in (0, n)
+                lost += int(1 <= s_full <= k - 1)
+            q = 1 - p[u] ** n_stop - (1 - p[u]) ** n_stop
+            want += n_stop + (k - n_stop) * q
+            var += (k - n_stop) ** 2 * q * (1 - q)
         assert abs(st["rollouts"] - want) <= 5 * math.sqrt(var) + 1e-9
         ab = drawn - st["committed"]
-        rows.append((tau, n_a, drawn, st["rollouts"] / drawn, st["rollouts"] / max(st["committed"], 1),
-                     st["committed"], 100.0 * lost / max(ab, 1), 100.0 * (1 - lost / drawn)))
-    print("[tau sweep] tau n_a drawn rollouts/drawn rollouts/effective committed lost% quality%", flush=True)
+        return (k, n0, tau, n_stop, drawn, st["rollouts"] / drawn, st["rollouts"] / max(st["committed"], 1),
+                st["committed"], 100.0 * lost / max(ab, 1), 100.0 * (1 - lost / drawn), st["decode_steps"])
+
+    rows = [point(8, 2, tau) for tau in (0.1, 0.3, 0.45, 0.6)]
+    rows += [point(8, n0, 0.45) for n0 in (1, 4)]
+    rows += [point(k, 2, 0.45) for k in (4, 16)]
+    print("[sweep] k n0 tau n_stop drawn rollouts/drawn rollouts/effective committed lost% quality% "
+          "decode_steps", flush=True)
     for r in rows:
-        print("[tau sweep] %.2f %d %d %.3f %.2f %d %.1f %.1f" % r, flush=True)
+        print("[sweep] %d %d %.2f %d %d %.3f %.2f %d %.1f %.1f %d" % r, flush=True)
     # a higher threshold abandons sooner: fewer rollouts per drawn prompt
-    per = [r[3] for r in rows]
+    per = [r[5] for r in rows[:4]]
     assert all(a > b for a, b in zip(per, per[1:]))
