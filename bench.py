@@ -117,8 +117,9 @@ def main():
                          "step 0 from the HIP graph (for kernel traces), then exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the allocation step is "
-              f"single-GPU by design (see DESIGN.md, 'More than one GPU').", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the allocation step would "
+              f"shard by prompts (a model replica, slot pool and controller per GPU, no traffic "
+              f"inside a step), which this benchmark does not launch.", file=sys.stderr)
         sys.exit(2)
 
     import torch

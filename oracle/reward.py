@@ -8,8 +8,9 @@ SplitMix64 output finalizer (Steele, Lea, Flood, OOPSLA'14),
     reward = [ (h >> 11) * 2^-53 < p_uid ]        (exact in fp64),
 
 with seed_r = seed XOR 0xD1B54A32D192ED03.  The rollout index j is not hashed,
-so identical responses to one prompt earn identical rewards.  The definition is
-this build's own (parity unpinned by the paper); tests pin the two codings
+so identical responses to one prompt earn identical rewards.  The paper gives
+no such function, so this definition is our own (parity unpinned by the
+paper); tests pin the two codings
 below against each other and the reward frequency against p.
 """
 import numpy as np

@@ -270,7 +270,7 @@ def test_early_commit_expected_rollouts_eq_en(g):
 
 @pytest.mark.parametrize("m", [2, 3, 4])
 def test_commit_floor_mixture_rollouts(m):
-    """Commit floor m under the survey's success-rate mixture: E[N] =
+    """Commit floor m under the workloads' success-rate mixture: E[N] =
     m + sum_{n=m}^{n_a-1} E[g^n + (1-g)^n]; commit probability 1 - E[g^4 + (1-g)^4]
     for every floor m <= n_a (mixing is absorbing, the abandonment point is unchanged)."""
     U = 20000
