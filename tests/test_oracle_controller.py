@@ -288,3 +288,28 @@ def test_commit_floor_mixture_rollouts(m):
     if m < n_a:
         assert len(set(sizes)) > 1
     check_invariants(a, res, U)
+
+
+@pytest.mark.parametrize("k,n0,tau", [(8, 2, 0.1), (8, 2, 0.3), (8, 2, 0.6), (8, 1, 0.45), (8, 4, 0.45),
+                                      (4, 2, 0.45), (16, 2, 0.45), (8, 6, 0.45)])
+def test_ablation_stopping_times_under_mixture(k, n0, tau):
+    """tau, n0 and k ablations (commit floor k): an unmixed prompt stops at
+    n_stop = max(n0, n_a), n_a = k - floor(tau (k+1)) (Theorem 2's proof under
+    the uniform prior), a prompt mixed by then runs to k, so the rollouts per
+    drawn prompt are n_stop + (k - n_stop)(1 - E[g^n_stop + (1-g)^n_stop])."""
+    U = 12000
+    p = mixture_p(U, 31)
+    a = alloc(k=k, n0=n0, commit_min=k, tau_low=tau, B=10 ** 6, budget_N=10 ** 8, n_slots=4096)
+    res = C.simulate(a, U, synthetic(p, seed=13))
+    n_a = min(k, k - math.floor(tau * (k + 1)))
+    n_stop = max(n0, n_a)
+    pc = 1 - moment(n_stop, 0)
+    assert abs(res["n_committed"] / U - pc) < 5 * math.sqrt(pc * (1 - pc) / U)
+    want = n_stop + (k - n_stop) * pc
+    assert abs(res["rollouts"] / U - want) < 5 * (k - n_stop) * math.sqrt(pc * (1 - pc) / U) + 1e-12
+    for u in range(U):
+        if res["status"][u] == C.ABANDONED:
+            assert res["n_done"][u] == n_stop and res["successes"][u] in (0, n_stop)
+        else:
+            assert res["n_done"][u] == k
+    check_invariants(a, res, U)
