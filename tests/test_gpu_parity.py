@@ -454,3 +454,48 @@ def test_ablation_sweeps_with_exact_counterfactuals(torch_cuda):
     # a higher threshold abandons sooner: fewer rollouts per drawn prompt
     per = [r[5] for r in rows[:4]]
     assert all(a > b for a, b in zip(per, per[1:]))
+
+
+@pytest.mark.parametrize("variant", ["warm_start", "thompson"])
+def test_graph_replay_matches_eager_over_steps(torch_cuda, variant):
+    """The captured decode / decide / refill graph and the eager calls give
+    the same step, step after step, with warm-start priors carried between
+    steps or with the posterior-sampling priority on binding slots (fp32
+    model, three steps, free-running tokens): identical tokens, logs and
+    counts, and (warm start) identical carried pseudo-counts."""
+    from oracle import warm as OW  # noqa: F401  (the reading both paths implement)
+    torch = torch_cuda
+    cfg = W.get_config("tiny_f32")
+    cfg["alloc"].update(B=8, budget_N=64, pool_U=24, n_slots=64 if variant == "warm_start" else 6, max_new=16)
+    if variant == "thompson":
+        cfg["alloc"]["mode"] = "sara_thompson"
+    w = W.make_weights(cfg)
+    D = 48
+    pset = W.prompt_set(cfg, D)
+    runs = []
+    for use_graph in (False, True):
+        ctx, _ = device_setup(cfg, w)
+        d_a = torch.zeros(D, dtype=torch.float64, device="cuda")
+        d_b = torch.zeros(D, dtype=torch.float64, device="cuda")
+        out = []
+        for step in range(3):
+            pool = W.set_pool(cfg, pset, step)
+            d_ids = torch.from_numpy(pool["ids"]).cuda()
+            if variant == "warm_start":
+                ctx.sara_set_warm_start(d_ids, d_a, d_b)
+            g = run_gpu_step(ctx, cfg, pool, use_graph=use_graph)
+            if variant == "warm_start":
+                ctx.sara_warm_start_update(0.5)
+            torch.cuda.synchronize()
+            out.append((g, d_a.cpu().numpy().copy(), d_b.cpu().numpy().copy()))
+        ctx.close()
+        runs.append(out)
+    for step, ((ge, ae, be), (gg, ag, bg)) in enumerate(zip(*runs)):
+        for key in ("decisions", "draws", "assigns", "finishes"):
+            assert np.array_equal(ge["logs"][key], gg["logs"][key]), (step, key)
+        assert np.array_equal(ge["roll"]["tokens"], gg["roll"]["tokens"]), step
+        for f in ("committed", "rollouts", "tokens", "decode_steps", "budget_left"):
+            assert ge["stats"][f] == gg["stats"][f], (step, f)
+        assert np.array_equal(ae, ag) and np.array_equal(be, bg)
+    if variant == "warm_start":
+        assert np.any(runs[0][-1][1] > 0) or np.any(runs[0][-1][2] > 0)
