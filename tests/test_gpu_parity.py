@@ -175,7 +175,8 @@ def _model_free_case(cfg, U_tokens_seed=3):
                                        ("pool_3b", "sara"), ("pool_3b", "fixed_k"),
                                        ("qwen3b_shape", "sara"),
                                        ("qwen1p5b_shape", "commit_min=2"), ("qwen1p5b_shape", "commit_min=4"),
-                                       ("long_ragged_1p5b", "sara_thompson")])
+                                       ("long_ragged_1p5b", "sara_thompson"),
+                                       ("long_ragged_1p5b", "step=150"), ("long_ragged_1p5b", "step=299")])
 def test_controller_full_size_model_free(torch_cuda, name, mode):
     """Full-size allocation parameters of each workload; tokens from a table
     (decoder skipped), so the controller, hash reward and termination are
@@ -185,7 +186,8 @@ def test_controller_full_size_model_free(torch_cuda, name, mode):
     of 2..8 rollouts, so the GRPO advantages run over variable group sizes.
     The sara_thompson case orders pending rollouts by the posterior-sampling
     index on the workload whose 256 slots bind, so its assignment log differs
-    from the p_eff ordering's and must still match the oracle exactly."""
+    from the p_eff ordering's and must still match the oracle exactly.  The
+    step= cases run later steps of the drifting long-rollout workload."""
     full = W.get_config(name)
     if mode == "fixed_k":
         full = W.fixed_k_variant(full)
@@ -193,6 +195,7 @@ def test_controller_full_size_model_free(torch_cuda, name, mode):
         full["alloc"]["commit_min"] = int(mode.split("=")[1])
     elif mode == "sara_thompson":
         full["alloc"]["mode"] = "sara_thompson"
+    step = int(mode.split("=")[1]) if mode.startswith("step=") else 0
     cfg = W.get_config("tiny_f32")
     cfg["alloc"] = dict(full["alloc"])
     cfg["alloc"]["max_prompt"] = 32
@@ -206,7 +209,9 @@ def test_controller_full_size_model_free(torch_cuda, name, mode):
     a["max_new"] = min(a["max_new"], 96)
     if cfg["forced_len"] is not None:
         cfg["forced_len"] = dict(cfg["forced_len"], cap=a["max_new"], mu=math.log(40.0))
-    pool = W.make_pool(cfg, 0)
+    # later steps of the drifting workload: other success-rate weights, the
+    # step index in the sampler key and the reward hash
+    pool = W.make_pool(cfg, step)
     tab = _model_free_case(cfg)
     # EOS in the table ends rollouts early: sprinkle it with probability 1/40
     g = np.random.default_rng(9)
