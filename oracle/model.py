@@ -19,9 +19,10 @@ and accumulation stay wide.  GEMMs with bf16 operands accumulate in fp32
 Clock: prefill computes K/V for prompt positions 0..P-2; generated token i
 takes prompt[P-1] (i = 0) or token i-1 as input at position P-1+i.
 
-Parity unpinned by the paper (it prints no logits).  Pinned by tests against
-an independent torch-CPU functional forward, against full causal recompute
-of decode logits, and by the bf16 rounding against torch's conversion.
+The paper prints no logits to compare with; the decoder is pinned instead
+by tests against an independent torch-CPU functional forward (library
+attention and activations), against a full causal recompute of the decode
+logits, and by the bf16 rounding against torch's conversion.
 """
 import numpy as np
 

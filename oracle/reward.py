@@ -9,9 +9,9 @@ SplitMix64 output finalizer (Steele, Lea, Flood, OOPSLA'14),
 
 with seed_r = seed XOR 0xD1B54A32D192ED03.  The rollout index j is not hashed,
 so identical responses to one prompt earn identical rewards.  The paper gives
-no such function, so this definition is our own (parity unpinned by the
-paper); tests pin the two codings
-below against each other and the reward frequency against p.
+no such function, so the chain is our own definition: the mixing function is
+pinned by SplitMix64's published outputs and the reward frequency against p;
+tests also check the two codings below against each other.
 """
 import numpy as np
 
