@@ -13,7 +13,8 @@ stated reading of it) defines, with no blocking or fusion:
 * ``controller`` - one allocation step (Algorithm 1) as a slot-pool event
                    simulation on the decode-step clock.
 * ``philox``     - Philox4x32-10 counter-based generator (Salmon et al., SC'11).
-* ``sampler``    - temperature + Gumbel-max token draw, forced-EOS draw.
+* ``sampler``    - temperature + Gumbel-max token draw over the top-p
+                   nucleus, forced-EOS draw.
 * ``reward``     - synthetic verifiable reward: SplitMix64-finalizer hash chain
                    over the generated tokens, thresholded against p_uid.
 * ``model``      - pre-norm GQA decoder (RMSNorm, RoPE, SwiGLU) with bf16

@@ -88,7 +88,7 @@ class RolloutSource:
                     samp = tok
                 else:
                     samp, sc = sampler.sample(logits[ri], a["temperature"], self.seed,
-                                              self.step, r["rid"], i)
+                                              self.step, r["rid"], i, a.get("top_p", 1.0))
                     if sampler.near_tie(sc):
                         r["ties"] += 1
                     if self.keep_logits is not None and self.keep_logits(r["u"], r["j"], i):

@@ -14,7 +14,20 @@ Uniform from a word w: u = ((w >> 8) + 1/2) * 2^-24, exact and inside (0, 1).
 Gumbel noise: g = -log(-log u) evaluated in fp64 and rounded to fp32.
 Score: fp32(logit / T) + g in fp32; the token is the lowest id attaining the
 maximum score.  Forced EOS fires when word 0 < forced_eos_u32.
+
+Top-p (nucleus, Holtzman et al., ICLR'20) for top_p < 1: sort the vocabulary
+by probability, largest first, and keep the shortest prefix whose mass reaches
+top_p, together with every id tied with the last one kept; the Gumbel-max draw
+then runs over that set only (a draw from the renormalised truncated
+softmax).  Reading of "mass", fixed so that the cut is an integer decision:
+z_v = fp32(logit_v / T) (+0 for a zero), weight q_v = floor(exp(z_v - z_max)
+* 2^44) in fp64 then as an integer (the largest weight is 2^44), Q = sum of
+q_v, target t = ceil(fp64(top_p) * fp64(Q)); the nucleus is {v : z_v >= z*}
+with z* the largest z value whose set {z_v >= z*} holds weight >= t.
+top_p = 1 keeps the whole vocabulary (no weight is dropped).
 """
+import math
+
 import numpy as np
 
 from .philox import philox4x32
@@ -41,10 +54,68 @@ def scores(logits32: np.ndarray, temperature: float, g: np.ndarray) -> np.ndarra
     return (s + g).astype(np.float32)
 
 
-def sample(logits32, temperature, seed, step, rid, pos):
-    """Returns (token, score array) for one (rollout, position)."""
+NUCLEUS_FRAC_BITS = 44
+
+
+def nucleus_weights(logits32, temperature):
+    """(z, integer weights q) of the top-p reading in the module header."""
+    z = (np.asarray(logits32, dtype=np.float32) / np.float32(temperature)).astype(np.float32)
+    z = np.where(z == 0, np.float32(0.0), z).astype(np.float32)
+    e = np.exp(z.astype(np.float64) - np.float64(z.max()))
+    q = [int(x) for x in np.floor(e * 2.0 ** NUCLEUS_FRAC_BITS)]
+    return z, q
+
+
+def nucleus_target(top_p: float, Q: int) -> int:
+    return int(math.ceil(float(np.float64(np.float32(top_p))) * float(Q)))
+
+
+def nucleus(logits32, temperature, top_p):
+    """Boolean mask of the top-p nucleus over the vocabulary."""
+    V = len(logits32)
+    if np.float32(top_p) >= 1:
+        return np.ones(V, dtype=bool)
+    z, q = nucleus_weights(logits32, temperature)
+    t = nucleus_target(top_p, sum(q))
+    order = sorted(range(V), key=lambda v: -float(z[v]))
+    cum = 0
+    pos = 0
+    while pos < V:
+        # one group of equal z values, all taken together
+        end = pos
+        while end < V and z[order[end]] == z[order[pos]]:
+            cum += q[order[end]]
+            end += 1
+        if cum >= t:
+            return z >= z[order[pos]]
+        pos = end
+    raise AssertionError("the weights of the whole vocabulary reach any target")
+
+
+def nucleus_margin(logits32, temperature, top_p) -> float:
+    """Distance of the cut from the target, as a fraction of the total weight:
+    how far the kept weight exceeds t, and how far the weight above the cut
+    group falls short of it (the smaller of the two).  A cut decided by less
+    than a few units of the last place of exp is reported near 0."""
+    if np.float32(top_p) >= 1:
+        return 1.0
+    z, q = nucleus_weights(logits32, temperature)
+    Q = sum(q)
+    t = nucleus_target(top_p, Q)
+    m = nucleus(logits32, temperature, top_p)
+    kept = sum(qv for qv, keep in zip(q, m) if keep)
+    zc = float(np.min(z[m]))
+    above = sum(qv for qv, zv in zip(q, z) if zv > zc)
+    return min(kept - t, t - 1 - above) / Q
+
+
+def sample(logits32, temperature, seed, step, rid, pos, top_p=1.0):
+    """Returns (token, score array) for one (rollout, position); ids outside
+    the top-p nucleus get score -inf."""
     V = len(logits32)
     sc = scores(logits32, temperature, gumbel(seed, step, rid, pos, V))
+    if np.float32(top_p) < 1:
+        sc = np.where(nucleus(logits32, temperature, top_p), sc, np.float32(-np.inf)).astype(np.float32)
     return int(np.argmax(sc)), sc
 
 
@@ -60,4 +131,6 @@ def forced_eos(seed, step, rid, pos, thresh_u32: int) -> bool:
 def near_tie(sc: np.ndarray, rel: float = 1e-5) -> bool:
     """True when the two best scores are within rel * max(1, |best|)."""
     top = np.partition(sc.astype(np.float64), -2)[-2:]
+    if not np.isfinite(top[0]):
+        return False
     return (top[1] - top[0]) <= rel * max(1.0, abs(top[1]))

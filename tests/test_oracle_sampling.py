@@ -119,3 +119,96 @@ def test_grpo_matches_library_statistics():
             assert np.allclose(a[lo:hi], (x - x.mean()) / (x.std(ddof=1) + 1e-6))
         else:
             assert np.all(a[lo:hi] == 0)
+
+
+# --- top-p nucleus -----------------------------------------------------------
+
+def _nucleus_by_prefix(logits, T, top_p):
+    """The nucleus by its plain definition, in 50-digit arithmetic: walk the
+    ids by (probability desc, id asc) and stop at the first prefix whose mass
+    reaches top_p, then add every id tied with the last one."""
+    import mpmath
+    mpmath.mp.dps = 50
+    z = [mpmath.mpf(float(np.float32(np.float32(x) / np.float32(T)))) for x in logits]
+    zmax = max(z)
+    w = [mpmath.e ** (zi - zmax) for zi in z]
+    tot = sum(w)
+    order = sorted(range(len(z)), key=lambda v: (-w[v], v))
+    cum = mpmath.mpf(0)
+    target = mpmath.mpf(float(np.float32(top_p)))
+    for n, v in enumerate(order):
+        cum += w[v] / tot
+        if cum >= target:
+            cut = w[v]
+            return np.array([wi >= cut for wi in w]), float(abs(cum - target))
+    raise AssertionError
+
+
+def test_nucleus_matches_the_prefix_definition():
+    rng = np.random.default_rng(11)
+    checked = 0
+    for trial in range(60):
+        V = int(rng.integers(2, 40))
+        logits = (rng.standard_normal(V) * rng.choice([0.3, 1.0, 3.0])).astype(np.float32)
+        if trial % 5 == 0:   # exact ties, also at the cut
+            logits[rng.integers(0, V, size=V // 2)] = logits[0]
+        T = float(rng.choice([1.0, 0.7, 1.3]))
+        top_p = float(rng.choice([0.05, 0.3, 0.5, 0.9, 0.95, 0.999]))
+        want, gap = _nucleus_by_prefix(logits, T, top_p)
+        if gap < 1e-9:
+            continue
+        got = sampler.nucleus(logits, T, top_p)
+        assert np.array_equal(got, want), (trial, logits, T, top_p)
+        assert sampler.nucleus_margin(logits, T, top_p) > 0
+        checked += 1
+    assert checked >= 50
+
+
+def test_nucleus_ties_at_the_cut_are_kept():
+    # p = (0.4, 0.2, 0.2, 0.2): at top_p 0.5 the prefix stops inside the tie
+    logits = np.log(np.array([2.0, 1.0, 1.0, 1.0])).astype(np.float32)
+    m = sampler.nucleus(logits, 1.0, 0.5)
+    assert m.tolist() == [True, True, True, True]
+    assert sampler.nucleus(logits, 1.0, 0.3).tolist() == [True, False, False, False]
+
+
+def test_nucleus_limits():
+    rng = np.random.default_rng(3)
+    logits = rng.standard_normal(300).astype(np.float32)
+    # top_p = 1 keeps every id, also those whose weight is below 2^-44
+    logits[7] = -200.0
+    assert sampler.nucleus(logits, 1.0, 1.0).all()
+    # a tiny top_p keeps only the most likely id (greedy)
+    m = sampler.nucleus(logits, 1.0, 1e-7)
+    assert m.sum() == 1 and m[int(np.argmax(logits))]
+    # the nucleus is minimal: its mass reaches top_p, without its cut group it does not
+    p = np.exp(logits.astype(np.float64) - logits.max())
+    p /= p.sum()
+    for top_p in (0.2, 0.6, 0.9):
+        m = sampler.nucleus(logits, 1.0, top_p)
+        zc = logits[m].min()
+        assert p[m].sum() >= top_p - 1e-12
+        assert p[logits > zc].sum() < top_p
+        # the sample never leaves the nucleus
+        for rid in range(50):
+            tok, sc = sampler.sample(logits, 1.0, 5, 0, rid, 1, top_p)
+            assert m[tok]
+            assert np.isneginf(sc[~m]).all()
+
+
+def test_top_p_sampling_is_truncated_softmax():
+    V = 12
+    logits = np.linspace(-1.5, 1.0, V).astype(np.float32)
+    T, top_p = 0.9, 0.8
+    m = sampler.nucleus(logits, T, top_p)
+    assert 2 <= m.sum() < V
+    p = np.where(m, np.exp(logits.astype(np.float64) / T), 0.0)
+    p /= p.sum()
+    n = 20000
+    toks = np.array([sampler.sample(logits, T, 321, 2, rid, 0, top_p)[0] for rid in range(n)])
+    obs = np.bincount(toks, minlength=V)
+    assert obs[~m].sum() == 0
+    assert stats.chisquare(obs[m], p[m] * n).pvalue > 1e-4
+    # top_p = 1 is the plain sampler, token for token
+    for rid in range(200):
+        assert sampler.sample(logits, T, 9, 0, rid, 4, 1.0)[0] == sampler.sample(logits, T, 9, 0, rid, 4)[0]
