@@ -84,7 +84,13 @@ typedef struct {
  *   pool_U      prompts in the step's pool;  n_slots concurrent rollout slots
  *   kv_block    KV page size in tokens (must be 16)
  *   max_prompt  longest prompt;  max_new  generated-token cap per rollout
- *   temperature sampling temperature (> 0);  top_p must be 1 (full softmax)
+ *   temperature sampling temperature (> 0);  top_p in (0, 1]: 1 samples the
+ *               full softmax, < 1 the top-p nucleus (smallest set of most
+ *               likely ids whose probability mass reaches top_p, with every
+ *               id tied at the cut; mass counted in integer weights
+ *               floor(exp(z - z_max) * 2^44) of z = fp32(logit / T)).  The
+ *               nucleus path writes fp32 logits [n_slots][vocab] (library
+ *               memory for bf16 models) and runs a separate sampler kernel
  *   forced_eos_u32  per-token probability x / 2^32 of a forced EOS (0 = off)
  *   prio_quant_bits  quantisation of the p_eff priority key (1..21)
  *   seed        key material of the counter-based sampler and reward hash
@@ -257,11 +263,12 @@ int grpo_group_advantages(const float* d_r, const int32_t* d_group_off, int32_t 
 
 /* Sampler alone, for parity on given logits: rows r < n_rows, logits
  * d_logits[r][vocab] fp32, rollout ids d_rid[r], generated indices d_pos[r]
- * -> d_tok[r] (Gumbel-max at temperature, forced EOS if eos_id >= 0 and
- * forced_eos_u32 > 0).  Enqueued on stream. */
+ * -> d_tok[r] (Gumbel-max at temperature over the top-p nucleus, the whole
+ * vocabulary when top_p = 1; forced EOS if eos_id >= 0 and forced_eos_u32 >
+ * 0).  top_p in (0, 1], else SARA_EINVAL.  Synchronises the stream. */
 int sara_sample_logits(const float* d_logits, int32_t n_rows, int32_t vocab,
                        const int32_t* d_rid, const int32_t* d_pos, uint64_t seed,
-                       int32_t step_index, float temperature, int32_t eos_id,
+                       int32_t step_index, float temperature, float top_p, int32_t eos_id,
                        uint32_t forced_eos_u32, int32_t* d_tok, void* stream);
 
 /* Self-check of the fused LM-head sampler (bf16 models).  That sampler

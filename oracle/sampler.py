@@ -58,11 +58,12 @@ NUCLEUS_FRAC_BITS = 44
 
 
 def nucleus_weights(logits32, temperature):
-    """(z, integer weights q) of the top-p reading in the module header."""
+    """(z, integer weights q as uint64) of the top-p reading in the module
+    header; q <= 2^44, so floor() of the fp64 product is exact."""
     z = (np.asarray(logits32, dtype=np.float32) / np.float32(temperature)).astype(np.float32)
     z = np.where(z == 0, np.float32(0.0), z).astype(np.float32)
     e = np.exp(z.astype(np.float64) - np.float64(z.max()))
-    q = [int(x) for x in np.floor(e * 2.0 ** NUCLEUS_FRAC_BITS)]
+    q = np.floor(e * 2.0 ** NUCLEUS_FRAC_BITS).astype(np.uint64)
     return z, q
 
 
@@ -71,25 +72,20 @@ def nucleus_target(top_p: float, Q: int) -> int:
 
 
 def nucleus(logits32, temperature, top_p):
-    """Boolean mask of the top-p nucleus over the vocabulary."""
+    """Boolean mask of the top-p nucleus over the vocabulary: walk the z
+    values from the largest down, one group of equal values at a time, and
+    stop at the first group after which the kept weight reaches t."""
     V = len(logits32)
     if np.float32(top_p) >= 1:
         return np.ones(V, dtype=bool)
     z, q = nucleus_weights(logits32, temperature)
-    t = nucleus_target(top_p, sum(q))
-    order = sorted(range(V), key=lambda v: -float(z[v]))
-    cum = 0
-    pos = 0
-    while pos < V:
-        # one group of equal z values, all taken together
-        end = pos
-        while end < V and z[order[end]] == z[order[pos]]:
-            cum += q[order[end]]
-            end += 1
-        if cum >= t:
-            return z >= z[order[pos]]
-        pos = end
-    raise AssertionError("the weights of the whole vocabulary reach any target")
+    t = nucleus_target(top_p, int(q.sum()))
+    order = np.argsort(-z, kind="stable")
+    zs = z[order]
+    cum = np.cumsum(q[order])                      # exact: total < 2^63
+    group_end = np.append(zs[1:] != zs[:-1], True)  # last position of each equal-z group
+    first = int(np.nonzero(group_end & (cum >= np.uint64(t)))[0][0])
+    return z >= zs[first]
 
 
 def nucleus_margin(logits32, temperature, top_p) -> float:
@@ -100,12 +96,11 @@ def nucleus_margin(logits32, temperature, top_p) -> float:
     if np.float32(top_p) >= 1:
         return 1.0
     z, q = nucleus_weights(logits32, temperature)
-    Q = sum(q)
+    Q = int(q.sum())
     t = nucleus_target(top_p, Q)
     m = nucleus(logits32, temperature, top_p)
-    kept = sum(qv for qv, keep in zip(q, m) if keep)
-    zc = float(np.min(z[m]))
-    above = sum(qv for qv, zv in zip(q, z) if zv > zc)
+    kept = int(q[m].sum())
+    above = int(q[z > np.min(z[m])].sum())
     return min(kept - t, t - 1 - above) / Q
 
 

@@ -80,7 +80,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "sara_read_advantages": [P, P, P, P, I32],
         "sara_peff_batch": [P, P, I32, F64, F64, I32, P, P],
         "grpo_group_advantages": [P, P, I32, F32, P, P],
-        "sara_sample_logits": [P, I32, I32, P, P, U64, I32, F32, I32, ctypes.c_uint32, P, P],
+        "sara_sample_logits": [P, I32, I32, P, P, U64, I32, F32, F32, I32, ctypes.c_uint32, P, P],
         "sara_gumbel_fast_max_error": [ctypes.POINTER(F64), P],
         "sara_set_profiling": [P, I32],
         "sara_reset_profile": [P],
@@ -321,9 +321,9 @@ def sara_gumbel_fast_max_error(stream=None):
 
 
 def sara_sample_logits(d_logits, d_rid, d_pos, seed, step_index, temperature, eos_id, forced_eos_u32,
-                       d_tok, stream=None):
+                       d_tok, stream=None, top_p=1.0):
     n, V = d_logits.shape
     _check(_lib.sara_sample_logits(_ptr(d_logits), int(n), int(V), _ptr(d_rid), _ptr(d_pos),
                                    int(seed) & ((1 << 64) - 1), int(step_index), float(temperature),
-                                   int(eos_id), int(forced_eos_u32), _ptr(d_tok), _stream_handle(stream)),
+                                   float(top_p), int(eos_id), int(forced_eos_u32), _ptr(d_tok), _stream_handle(stream)),
            "sara_sample_logits")

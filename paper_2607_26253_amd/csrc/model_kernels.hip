@@ -1603,11 +1603,163 @@ __global__ __launch_bounds__(256) void k_sample_partial(const int32_t* __restric
   }
 }
 
-__device__ __forceinline__ int reduce_chunks(const float* best, const int32_t* bidx, int i) {
+// ---------------------------------------------------------------------------
+// top-p (nucleus) sampler, top_p < 1 (nucleus sampling, Holtzman et al.):
+// one 1024-thread block per row over its fp32 logits.  Mass is counted in
+// integer weights q_v = floor(exp(z_v - z_max) * 2^44), z_v = fp32(logit_v /
+// T), so the cut is an exact integer decision whatever the order of the
+// sums: the nucleus is {v : z_v >= z*}, with z* the largest z whose upper set
+// holds weight >= t = ceil(top_p * Q), Q the total weight; every id tied with
+// the cut is kept.  z* comes from a three-pass radix descent over the
+// order-preserving bits of z (11, 11 and 10 bits) with integer histograms in
+// LDS; the draw is then the Gumbel-max of the full sampler restricted to the
+// nucleus (lowest id on ties).  The row's logits (4 B per id) are read five
+// times, from L2 after the first pass.
+// ---------------------------------------------------------------------------
+constexpr int kTopPThreads = 1024;
+constexpr int kTopPWaves = kTopPThreads / 64;
+constexpr int kTopPBins = 2048;
+
+__device__ __forceinline__ uint32_t zkey(float z) {
+  uint32_t u = __float_as_uint(z);
+  if ((u & 0x7FFFFFFFu) == 0u) u = 0u;   // -0 and +0 are one value
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ uint64_t nucleus_weight(float z, float zmax) {
+  return (uint64_t)floor(ldexp(exp((double)z - (double)zmax), 44));
+}
+
+__global__ __launch_bounds__(kTopPThreads) void k_sample_topp(const int32_t* __restrict__ M_ptr,
+    const int32_t* __restrict__ rid_arr, const int32_t* __restrict__ pos_arr,
+    const RowDesc* __restrict__ rows, const float* __restrict__ logits, int V, int by_slot,
+    const CtlParams* __restrict__ cpd, uint64_t seed, int32_t step, float temp, float top_p,
+    float* __restrict__ best, int32_t* __restrict__ bidx, int rstride) {
+  __shared__ unsigned long long hist[kTopPBins];
+  __shared__ unsigned long long wsum[kTopPWaves];
+  __shared__ float wmax[kTopPWaves];
+  __shared__ int widx[kTopPWaves];
+  __shared__ unsigned long long sel_above, target;
+  __shared__ uint32_t sel_digit;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (cpd) { seed = cpd->seed; step = cpd->step; temp = cpd->temperature; top_p = cpd->top_p; }
+  uint32_t k0, k1;
+  sampler_key(seed, step, k0, k1);
+  const int M = *M_ptr;
+  for (int i = blockIdx.x; i < M; i += gridDim.x) {
+    const int rid = rows ? rows[i].rid : rid_arr[i];
+    const int gen = rows ? rows[i].gen : pos_arr[i];
+    const float* lg = logits + (size_t)(by_slot ? rows[i].slot : i) * V;
+    // z_max
+    float zm = -INFINITY;
+    for (int v = tid; v < V; v += kTopPThreads) zm = fmaxf(zm, __fdiv_rn(lg[v], temp));
+    zm = wave_max(zm);
+    if (lane == 0) wmax[wave] = zm;
+    __syncthreads();
+    zm = wmax[0];
+#pragma unroll
+    for (int w = 1; w < kTopPWaves; ++w) zm = fmaxf(zm, wmax[w]);
+    // radix descent: prefix holds the bits of z*'s key decided so far
+    uint32_t prefix = 0u;
+    unsigned long long above = 0ull;   // weight of keys above the current range
+#pragma unroll 1
+    for (int pass = 0; pass < 3; ++pass) {
+      const int sh = (pass == 0) ? 21 : (pass == 1 ? 10 : 0);
+      const uint32_t dmask = (pass == 2) ? 1023u : 2047u;
+      hist[2 * tid] = 0ull;
+      hist[2 * tid + 1] = 0ull;
+      __syncthreads();
+      unsigned long long tot = 0ull;
+      for (int v = tid; v < V; v += kTopPThreads) {
+        const float z = __fdiv_rn(lg[v], temp);
+        const uint32_t key = zkey(z);
+        // the bits decided so far: 31..21 after pass 0, 31..10 after pass 1
+        const int hi = (pass == 1) ? 21 : 10;
+        const bool in = (pass == 0) || ((key >> hi) == (prefix >> hi));
+        if (in) {
+          const uint64_t q = nucleus_weight(z, zm);
+          tot += q;
+          if (q) atomicAdd(&hist[(key >> sh) & dmask], (unsigned long long)q);
+        }
+      }
+      if (pass == 0) {
+        // total weight and target t = ceil(top_p * Q)
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) tot += __shfl_xor(tot, o, 64);
+        if (lane == 0) wsum[wave] = tot;
+      }
+      __syncthreads();
+      if (pass == 0 && tid == 0) {
+        unsigned long long Q = 0ull;
+        for (int w = 0; w < kTopPWaves; ++w) Q += wsum[w];
+        target = (unsigned long long)ceil((double)top_p * (double)Q);
+      }
+      // suffix sums of the histogram: thread t owns bins 2t and 2t+1
+      const unsigned long long h0 = hist[2 * tid], h1 = hist[2 * tid + 1];
+      unsigned long long incl = h0 + h1;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const unsigned long long y = __shfl_down(incl, o, 64);
+        if (lane + o < 64) incl += y;
+      }
+      __syncthreads();
+      if (lane == 0) wsum[wave] = incl;
+      __syncthreads();
+      unsigned long long excl = incl - (h0 + h1);
+      for (int w = wave + 1; w < kTopPWaves; ++w) excl += wsum[w];
+      // the one bin where the upper-set weight first reaches the target
+      const unsigned long long t = target;
+      const unsigned long long a1 = above + excl, a0 = a1 + h1;
+      if (a1 < t && a1 + h1 >= t) { sel_digit = 2 * tid + 1; sel_above = a1; }
+      if (a0 < t && a0 + h0 >= t) { sel_digit = 2 * tid; sel_above = a0; }
+      __syncthreads();
+      prefix |= sel_digit << sh;
+      above = sel_above;
+      __syncthreads();   // hist, wsum and the selection are rewritten next pass
+    }
+    // Gumbel-max over the nucleus {key >= prefix}
+    float bs = -INFINITY;
+    int bi = 0x7FFFFFFF;
+    const int nblk = (V + 3) >> 2;
+    for (int b = tid; b < nblk; b += kTopPThreads) {
+      float z[4];
+      bool any = false;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int v = 4 * b + e;
+        z[e] = (v < V) ? __fdiv_rn(lg[v], temp) : -INFINITY;
+        any |= (v < V) && zkey(z[e]) >= prefix;
+      }
+      if (!any) continue;
+      U32x4 w = philox4x32_10((uint32_t)rid, (uint32_t)gen, (uint32_t)b, 0u, k0, k1);
+      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int v = 4 * b + e;
+        if (v < V && zkey(z[e]) >= prefix) better(bs, bi, __fadd_rn(z[e], gumbel_exact(ws[e])), v);
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float s2 = __shfl_xor(bs, o, 64);
+      const int i2 = __shfl_xor(bi, o, 64);
+      better(bs, bi, s2, i2);
+    }
+    if (lane == 0) { wmax[wave] = bs; widx[wave] = bi; }
+    __syncthreads();
+    if (tid == 0) {
+      for (int w = 1; w < kTopPWaves; ++w) better(bs, bi, wmax[w], widx[w]);
+      best[(size_t)i * rstride] = bs;
+      bidx[(size_t)i * rstride] = bi;
+    }
+    __syncthreads();   // wmax/widx are reused by the next row
+  }
+}
+
+__device__ __forceinline__ int reduce_chunks(const float* best, const int32_t* bidx, int i, int nchunks) {
   float bs = -INFINITY;
   int bi = 0x7FFFFFFF;
-  for (int c = 0; c < kSampleChunks; ++c)
-    better(bs, bi, best[(size_t)i * kSampleChunks + c], bidx[(size_t)i * kSampleChunks + c]);
+  for (int c = 0; c < nchunks; ++c)
+    better(bs, bi, best[(size_t)i * nchunks + c], bidx[(size_t)i * nchunks + c]);
   return bi;
 }
 
@@ -1694,11 +1846,11 @@ __global__ __launch_bounds__(256) void k_sample_final(const Ctl* __restrict__ ct
 // stand-alone sampler for given logits (parity entry point)
 __global__ void k_sample_rows_final(int n_rows, const int32_t* __restrict__ rid,
     const int32_t* __restrict__ pos, const float* __restrict__ best,
-    const int32_t* __restrict__ bidx, uint64_t seed, int32_t step, int eos, uint32_t feos,
+    const int32_t* __restrict__ bidx, int nchunks, uint64_t seed, int32_t step, int eos, uint32_t feos,
     int32_t* __restrict__ tok) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n_rows) return;
-  int t = reduce_chunks(best, bidx, i);
+  int t = reduce_chunks(best, bidx, i, nchunks);
   if (eos >= 0 && forced_eos_fires(seed, step, rid[i], pos[i], feos)) t = eos;
   tok[i] = t;
 }
@@ -2018,12 +2170,24 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
       // exact winners, reduced by k_sample_final
       const int nb = (c->V + 127) / 128;
       nchunks = nb;
+      // top-p < 1: the GEMM also writes the logits ([slot][V]) for the
+      // nucleus sampler, whose winner replaces the epilogue's
+      float* lg_out = (c->topp && !logits) ? c->topp_logits : logits;
       PROF_B(c);
       launch_k(c, st, (k_gemm_bf16_lds<2, 8, 64, 2, 0>), dim3(nb, 1, 1), dim3(256), 0,
                          (const uint16_t*)c->x, (const uint16_t*)c->lm_head, (void*)nullptr, c->rows_M, c->V,
                          c->d, c->d, (int64_t)0,
-                         SampleArgs{c->rows, (const CtlParams*)c->cp_dev, logits, c->samp_best, c->samp_idx, S});
+                         SampleArgs{c->rows, (const CtlParams*)c->cp_dev, lg_out, c->samp_best, c->samp_idx, S});
       PROF_E(c, kPGemmLM, c->V, c->d);
+      if (c->topp) {
+        PROF_B(c);
+        launch_k(c, st, k_sample_topp, dim3(std::min(S, 1024)), dim3(kTopPThreads), 0, c->rows_M,
+                           (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, (const float*)lg_out, c->V, 1,
+                           (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, 1.0f, c->samp_best,
+                           c->samp_idx, 1);
+        PROF_E(c, kPSampleP, c->V, 0);
+        nchunks = 1;
+      }
     } else {
       layers<float>(c, c->rows_M, S, true);
       int sp;
@@ -2032,9 +2196,17 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
       gemm(c, c->x, c->lm_head, c->rows_M, S, c->V, c->d, sp, 1);
       PROF_E(c, kPGemmLM, c->V, c->d);
       PROF_B(c);
-      launch_k(c, st, k_sample_partial, dim3(std::min(S * kSampleChunks, 2048)), dim3(256), 0,
-                         c->rows_M, (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, c->ws, c->V,
-                         (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, c->samp_best, c->samp_idx);
+      if (c->topp) {
+        launch_k(c, st, k_sample_topp, dim3(std::min(S, 1024)), dim3(kTopPThreads), 0, c->rows_M,
+                           (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, (const float*)c->ws, c->V, 0,
+                           (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, 1.0f, c->samp_best,
+                           c->samp_idx, 1);
+        nchunks = 1;
+      } else {
+        launch_k(c, st, k_sample_partial, dim3(std::min(S * kSampleChunks, 2048)), dim3(256), 0,
+                           c->rows_M, (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, c->ws, c->V,
+                           (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, c->samp_best, c->samp_idx);
+      }
       PROF_E(c, kPSampleP, c->V, 0);
       if (logits) {
         PROF_B(c);
@@ -2046,7 +2218,8 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
   }
   PROF_B(c);
   // chunk winners: [row][kSampleChunks] from k_sample_partial, [chunk][S] from the fused LM head
-  const bool fused = !model_free && c->md.dtype == SARA_BF16;
+  // (one winner per row, at [row], from the nucleus sampler)
+  const bool fused = !model_free && c->md.dtype == SARA_BF16 && !c->topp;
   launch_k(c, st, k_sample_final, dim3(std::min(S, 1024)), dim3(256), 0, c->ctl, c->rows,
                      c->samp_best, c->samp_idx, nchunks, fused ? S : 1, fused ? 1 : nchunks, forced, c->flen,
                      model_free,
@@ -2057,7 +2230,7 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
 }
 
 int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* rid,
-                       const int32_t* pos, uint64_t seed, int step, float temp, int eos,
+                       const int32_t* pos, uint64_t seed, int step, float temp, float top_p, int eos,
                        uint32_t feos, int32_t* tok, hipStream_t st) {
   float* best = nullptr;
   int32_t* bidx = nullptr;
@@ -2070,12 +2243,18 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
   if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
   e = hipMemcpyAsync(mdev, &n_rows, sizeof(int32_t), hipMemcpyHostToDevice, st);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
-  hipLaunchKernelGGL(k_sample_partial, dim3(std::min(n_rows * kSampleChunks, 2048)), dim3(256), 0, st, mdev,
-                     rid, pos,
-                     (const RowDesc*)nullptr, logits, V, (const CtlParams*)nullptr, seed, step, temp,
-                     best, bidx);
+  const bool topp = top_p < 1.0f;
+  if (topp)
+    hipLaunchKernelGGL(k_sample_topp, dim3(std::min(n_rows, 1024)), dim3(kTopPThreads), 0, st, mdev, rid, pos,
+                       (const RowDesc*)nullptr, logits, V, 0, (const CtlParams*)nullptr, seed, step, temp,
+                       top_p, best, bidx, 1);
+  else
+    hipLaunchKernelGGL(k_sample_partial, dim3(std::min(n_rows * kSampleChunks, 2048)), dim3(256), 0, st, mdev,
+                       rid, pos,
+                       (const RowDesc*)nullptr, logits, V, (const CtlParams*)nullptr, seed, step, temp,
+                       best, bidx);
   hipLaunchKernelGGL(k_sample_rows_final, dim3((n_rows + 255) / 256), dim3(256), 0, st, n_rows, rid,
-                     pos, best, bidx, seed, step, eos, feos, tok);
+                     pos, best, bidx, topp ? 1 : kSampleChunks, seed, step, eos, feos, tok);
   (void)hipFreeAsync(best, st);
   (void)hipFreeAsync(bidx, st);
   (void)hipFreeAsync(mdev, st);

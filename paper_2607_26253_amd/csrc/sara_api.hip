@@ -177,7 +177,7 @@ static int validate(const sara_model_desc* m, const sara_alloc_desc* a) {
   if (a->mode != SARA_MODE_SARA && a->mode != SARA_MODE_FIXED_K && a->mode != SARA_MODE_SARA_THOMPSON)
     return einval("unknown mode");
   if (!(a->temperature > 0.f)) return einval("temperature must be > 0");
-  if (a->top_p != 1.0f) return einval("top_p must be 1 (nucleus truncation is not implemented)");
+  if (!(a->top_p > 0.f && a->top_p <= 1.f)) return einval("top_p must be in (0, 1]");
   if (a->prio_quant_bits < 1 || a->prio_quant_bits > 21) return einval("prio_quant_bits must be in [1, 21]");
   int64_t qcap = std::min<int64_t>(a->budget_N, (int64_t)a->pool_U * a->k);
   if (qcap > kMaxQueue) return einval("min(budget_N, pool_U*k) must be <= 4096");
@@ -305,6 +305,9 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   const size_t nchunk = std::max<size_t>(kSampleChunks, (size_t)(c->V + 127) / 128);
   ALLOC(c->samp_best, sizeof(float) * (size_t)c->S * nchunk);
   ALLOC(c->samp_idx, sizeof(int32_t) * (size_t)c->S * nchunk);
+  c->topp = c->ad.top_p < 1.0f;
+  // nucleus sampling reads fp32 logits; the bf16 LM head writes them here
+  if (c->topp && c->md.dtype == SARA_BF16) ALLOC(c->topp_logits, sizeof(float) * (size_t)c->S * c->V);
   ALLOC(c->g_off, sizeof(int32_t) * (c->U + 1));
   ALLOC(c->g_r, sizeof(float) * nroll);
   ALLOC(c->g_adv, sizeof(float) * nroll);
@@ -383,6 +386,7 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   p.tau = ad->tau_low; p.a0 = ad->alpha0; p.b0 = ad->beta0;
   p.prior = peff_host(0, 0, ad->k, ad->alpha0, ad->beta0);
   p.seed = ad->seed; p.step = 0; p.forced_eos = ad->forced_eos_u32; p.temperature = ad->temperature;
+  p.top_p = ad->top_p;
   p.has_flen = 0;
   e = hipMemcpyAsync(c->cp_dev, &p, sizeof(p), hipMemcpyHostToDevice, st);
   if (e == hipSuccess) e = hipStreamSynchronize(st);
@@ -705,14 +709,15 @@ extern "C" int grpo_group_advantages(const float* d_r, const int32_t* d_group_of
 
 extern "C" int sara_sample_logits(const float* d_logits, int32_t n_rows, int32_t vocab,
                                   const int32_t* d_rid, const int32_t* d_pos, uint64_t seed,
-                                  int32_t step_index, float temperature, int32_t eos_id,
+                                  int32_t step_index, float temperature, float top_p, int32_t eos_id,
                                   uint32_t forced_eos_u32, int32_t* d_tok, void* stream) {
   if (n_rows < 0 || vocab < 1) return einval("n_rows must be >= 0 and vocab >= 1");
   if (n_rows == 0) return SARA_OK;
   if (!d_logits || !d_rid || !d_pos || !d_tok) return einval("null array");
   if (!(temperature > 0.f)) return einval("temperature must be > 0");
+  if (!(top_p > 0.f && top_p <= 1.f)) return einval("top_p must be in (0, 1]");
   if (eos_id >= vocab) return einval("eos_id out of range");
-  return launch_sample_rows(d_logits, n_rows, vocab, d_rid, d_pos, seed, step_index, temperature, eos_id,
+  return launch_sample_rows(d_logits, n_rows, vocab, d_rid, d_pos, seed, step_index, temperature, top_p, eos_id,
                             forced_eos_u32, d_tok, (hipStream_t)stream);
 }
 

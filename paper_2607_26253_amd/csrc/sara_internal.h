@@ -72,6 +72,7 @@ struct CtlParams {
   int32_t step;
   uint32_t forced_eos;
   float temperature;
+  float top_p;                   // < 1: nucleus sampling over fp32 logits
   int32_t has_flen;
   int32_t has_prior;             // per-prompt priors (warm start) in place of (a0, b0, prior)
 };
@@ -154,6 +155,8 @@ struct sara_ctx {
   float* attn_part = nullptr;
   float* samp_best = nullptr;
   int32_t* samp_idx = nullptr;
+  bool topp = false;              // top_p < 1: nucleus sampler after the LM head
+  float* topp_logits = nullptr;   // [S][V] fp32 logits for it (bf16 models)
 
   // GRPO of committed groups
   int32_t* g_off = nullptr;
@@ -217,7 +220,7 @@ int launch_peff(const int32_t* n, const int32_t* s, int k, double a0, double b0,
 int launch_grpo(const float* r, const int32_t* off, int n_groups, float eps, float* adv,
                 hipStream_t st);
 int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* rid,
-                       const int32_t* pos, uint64_t seed, int step, float temp, int eos,
+                       const int32_t* pos, uint64_t seed, int step, float temp, float top_p, int eos,
                        uint32_t feos, int32_t* tok, hipStream_t st);
 int launch_convert_norms(sara_ctx* c, const void* const* w);
 int launch_gumbel_check(double* h_out, hipStream_t st);

@@ -49,7 +49,7 @@ def _descs(**over):
 
 
 @pytest.mark.parametrize("over", [dict(k=1), dict(n0=0), dict(n0=9), dict(commit_min=1), dict(tau_low=1.5),
-                                  dict(alpha0=0.0), dict(kv_block=8), dict(top_p=0.9), dict(head_dim=96),
+                                  dict(alpha0=0.0), dict(kv_block=8), dict(top_p=0.0), dict(top_p=1.5), dict(head_dim=96),
                                   dict(n_kv_heads=3), dict(temperature=0.0), dict(n_slots=0),
                                   dict(budget_N=10 ** 6, pool_U=10 ** 4), dict(prio_quant_bits=30),
                                   dict(eos_id=512)])
@@ -83,7 +83,11 @@ def test_pure_entry_points_validate_arguments():
     assert L.sara_peff_batch(None, None, 8, 0.0, 1.0, 0, None, None) == sara.SARA_EINVAL
     assert L.grpo_group_advantages(None, None, -2, 1e-6, None, None) == sara.SARA_EINVAL
     assert L.grpo_group_advantages(None, None, 3, 1e-6, None, None) == sara.SARA_EINVAL
-    assert L.sara_sample_logits(None, 4, 0, None, None, 0, 0, 1.0, -1, 0, None, None) == sara.SARA_EINVAL
+    assert L.sara_sample_logits(None, 4, 0, None, None, 0, 0, 1.0, 1.0, -1, 0, None, None) == sara.SARA_EINVAL
+    # top_p outside (0, 1] is refused before anything is enqueued
+    fake = ctypes.c_void_p(16)
+    for bad in (0.0, -0.5, 1.01):
+        assert L.sara_sample_logits(fake, 4, 512, fake, fake, 0, 0, 1.0, bad, -1, 0, fake, None) == sara.SARA_EINVAL
     assert L.sara_set_warm_start(None, None, None, None, 0) == sara.SARA_EINVAL
     assert L.sara_warm_start_update(None, 0.5) == sara.SARA_EINVAL
     assert L.sara_begin_step(None, None, None, None, None, 0) == sara.SARA_EINVAL

@@ -70,14 +70,16 @@ def check_sampler_on_oracle_logits(cfg, ora, seed, step):
     a, m = cfg["alloc"], cfg["model"]
     sara.sara_sample_logits(torch.from_numpy(lg).cuda(), torch.from_numpy(rid).cuda(),
                             torch.from_numpy(pos).cuda(), seed, step, a["temperature"],
-                            m["eos_id"], a["forced_eos_u32"], d_tok)
+                            m["eos_id"], a["forced_eos_u32"], d_tok, top_p=a.get("top_p", 1.0))
     got = d_tok.cpu().numpy()
     ties = 0
     for n, (u, j, i) in enumerate(keys):
         want = ora["rollouts_detail"][(u, j)]["sampled"][i]
         if got[n] != want:
-            _, sc = OS.sample(lg[n], a["temperature"], seed, step, int(rid[n]), i)
-            assert OS.near_tie(sc), (u, j, i, got[n], want)
+            tp = a.get("top_p", 1.0)
+            _, sc = OS.sample(lg[n], a["temperature"], seed, step, int(rid[n]), i, tp)
+            assert OS.near_tie(sc) or OS.nucleus_margin(lg[n], a["temperature"], tp) < 1e-8, \
+                (u, j, i, got[n], want)
             ties += 1
     assert ties <= 1
 
@@ -98,7 +100,7 @@ def check_fused_sampler_exact(cfg, gpu, seed, step):
     a, m = cfg["alloc"], cfg["model"]
     sara.sara_sample_logits(torch.from_numpy(lg).cuda(), torch.from_numpy(rid).cuda(),
                             torch.from_numpy(pos).cuda(), seed, step, a["temperature"],
-                            m["eos_id"], a["forced_eos_u32"], d_tok)
+                            m["eos_id"], a["forced_eos_u32"], d_tok, top_p=a.get("top_p", 1.0))
     want = d_tok.cpu().numpy()
     got = np.array([gpu["roll"]["sampled"][u * k + j][i] for _, (u, j, i) in rows])
     assert np.array_equal(got, want), np.nonzero(got != want)
@@ -162,6 +164,44 @@ def test_bf16_two_layer_truncation_strict(name):
     assert worst_max <= 3e-2
     check_fused_sampler_exact(cfg, gpu, seed, pool["step"])
     ctx.close()
+
+
+def test_bf16_two_layer_top_p():
+    """Nucleus sampling (top-p 0.9) on the bf16 decode path, 2 layers at the
+    1.5B shape's full width and vocabulary: the LM head writes its fp32
+    logits and the nucleus sampler draws from them.  Teacher forced: logs
+    bit-exact, logits <= 3e-2 * rms, the decode-path tokens equal the
+    stand-alone nucleus sampler's on the same GPU logits, and the sampler fed
+    the oracle's logits reproduces the oracle's tokens.  Free running with and
+    without a caller logits buffer (library buffer) gives the same rollouts."""
+    cfg = slice_cfg("qwen1p5b_shape", layers=2)
+    cfg["alloc"]["top_p"] = 0.9
+    w = W.make_weights(cfg)
+    pool = W.make_pool(cfg, 0)
+    seed = W.sampling_seed(cfg)
+    ora = ORUN.run_step(cfg, w, pool, seed, keep_logits=lambda u, j, i: True)
+    ctx, _ = device_setup(cfg, w)
+    gpu = run_gpu_step(ctx, cfg, pool, forced=forced_table(cfg, ora["rollouts_detail"]), capture_logits=True)
+    compare_logs(gpu["logs"], ora)
+    worst_max = max(e["max"] for e in row_errors(gpu, ora["logits"]))
+    assert worst_max <= 3e-2
+    n = check_fused_sampler_exact(cfg, gpu, seed, pool["step"])
+    check_sampler_on_oracle_logits(cfg, ora, seed, pool["step"])
+    print(f"[slice-2L-top-p] max|d|/rms {worst_max:.4f}; decode-path nucleus tokens = "
+          f"stand-alone sampler on {n} rows", flush=True)
+    ctx.close()
+    k = cfg["alloc"]["k"]
+    runs = []
+    for capture in (True, False):
+        ctx, _ = device_setup(cfg, w)
+        runs.append(run_gpu_step(ctx, cfg, pool, capture_logits=capture))
+        ctx.close()
+    a, b = runs
+    assert np.array_equal(a["logs"]["assigns"], b["logs"]["assigns"])
+    assert np.array_equal(a["logs"]["finishes"], b["logs"]["finishes"])
+    for (t, s, u, j, Ln, r) in a["logs"]["finishes"]:
+        rid = u * k + j
+        assert np.array_equal(a["roll"]["tokens"][rid][:Ln], b["roll"]["tokens"][rid][:Ln])
 
 
 def test_bf16_two_layer_long_context_strict():

@@ -93,6 +93,69 @@ def test_sampler_on_oracle_logits(torch_cuda, V):
         assert ties <= 1
 
 
+@pytest.mark.parametrize("V", [512, 151936])
+def test_top_p_sampler_on_given_logits(torch_cuda, V):
+    """Nucleus sampling through the stand-alone entry point against the
+    oracle's nucleus and Gumbel-max draw: every token equal, except where the
+    oracle's cut lies within 1e-8 of the total weight of its target (an exp
+    rounding apart) or the two best scores nearly tie."""
+    import paper_2607_26253_amd as sara
+    torch = torch_cuda
+    g = np.random.default_rng(V + 1)
+    n = 24 if V == 512 else 10
+    scale = np.where(np.arange(n) % 2 == 0, 0.8, 6.0)[:, None]
+    logits = (g.standard_normal((n, V)) * scale).astype(np.float32)
+    logits[1, : V // 3] = logits[1, 0]          # a large tie group
+    logits[3, g.integers(0, V, 64)] = logits[3].max()   # ties at the maximum
+    rid = np.arange(n, dtype=np.int32) * 5 + 2
+    pos = (np.arange(n, dtype=np.int32) * 11) % 1024
+    seed, step = W.sampling_seed(W.get_config("qwen1p5b_shape")), 3
+    cases = [(1.0, 0.9), (0.7, 0.5)] if V == 512 else [(1.0, 0.95), (1.0, 0.3)]
+    if V == 512:
+        cases.append((1.3, 1e-6))
+    for temp, top_p in cases:
+        d_tok = torch.empty(n, dtype=torch.int32, device="cuda")
+        sara.sara_sample_logits(torch.from_numpy(logits).cuda(), torch.from_numpy(rid).cuda(),
+                                torch.from_numpy(pos).cuda(), seed, step, temp, -1, 0, d_tok, top_p=top_p)
+        got = d_tok.cpu().numpy()
+        skipped = 0
+        for i in range(n):
+            tok, sc = OS.sample(logits[i], temp, seed, step, int(rid[i]), int(pos[i]), top_p)
+            assert OS.nucleus(logits[i], temp, top_p)[got[i]], (i, top_p)
+            if got[i] != tok:
+                assert OS.near_tie(sc) or OS.nucleus_margin(logits[i], temp, top_p) < 1e-8, (i, got[i], tok)
+                skipped += 1
+        print(f"[top-p] V={V} T={temp} top_p={top_p}: {n - skipped}/{n} rows equal", flush=True)
+        assert skipped <= 1
+
+
+def test_tiny_top_p_step_matches_oracle(torch_cuda):
+    """A whole allocation step of the fp32 model sampling from the top-p 0.9
+    nucleus: teacher-forced logits <= 1e-3, logs bit-exact, the sampler's own
+    tokens equal the oracle's, then free running from the captured graph
+    reproduces the oracle's rollouts token for token."""
+    cfg, w, pool, seed = _tiny()
+    cfg["alloc"].update(B=8, budget_N=64, pool_U=32, n_slots=64, max_new=32, top_p=0.9)
+    ora = ORUN.run_step(cfg, w, pool, seed, keep_logits=lambda u, j, i: True)
+    ctx, _ = device_setup(cfg, w)
+    gpu = run_gpu_step(ctx, cfg, pool, forced=forced_table(cfg, ora["rollouts_detail"]), capture_logits=True)
+    compare_logs(gpu["logs"], ora)
+    worst = max(float(np.max(np.abs(gpu["logits"][t][s] - ora["logits"][(u, j, i)])))
+                for (t, s), (u, j, i) in slot_rows(gpu).items())
+    assert worst <= 1e-3, worst
+    k = cfg["alloc"]["k"]
+    diff = sum(int(np.sum(gpu["roll"]["sampled"][u * k + j][:d["length"]] != d["tokens"]))
+               for (u, j), d in ora["rollouts_detail"].items())
+    assert diff <= 2
+    ctx.close()
+    ctx, _ = device_setup(cfg, w)
+    free = run_gpu_step(ctx, cfg, pool, use_graph=True)
+    for (u, j), d in ora["rollouts_detail"].items():
+        assert np.array_equal(free["roll"]["tokens"][u * k + j][:d["length"]], d["tokens"]), (u, j)
+    compare_logs(free["logs"], ora)
+    ctx.close()
+
+
 def _tiny():
     cfg = W.get_config("tiny_f32")
     w = W.make_weights(cfg)
