@@ -60,7 +60,7 @@ def describe(cfg):
     return (f"{cfg['name']}: {m['n_layers']}L d{m['d_model']} {m['n_heads']}Q/{m['n_kv_heads']}KV x{m['head_dim']} "
             f"ffn{m['d_ffn']} V{m['vocab']} {m['dtype']}; B={a['B']} k={a['k']} n0={a['n0']} tau={a['tau_low']} "
             f"N={a['budget_N']} slots={a['n_slots']} pool={a['pool_U']} prompts U{list(cfg['prompt_len'])} "
-            f"max_new={a['max_new']} mode={a['mode']}")
+            f"max_new={a['max_new']} mode={a['mode']}" + (f" top_p={a['top_p']}" if a.get("top_p", 1.0) != 1.0 else ""))
 
 
 def cpu_baseline(cfg, weights, seconds_target=15.0):
@@ -103,6 +103,12 @@ def main():
     ap.add_argument("--steps", type=int, default=2)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--config", default="qwen1p5b_shape")
+    ap.add_argument("--mode", default="sara", choices=["sara", "fixed_k", "sara_thompson"],
+                    help="allocation rule: SARA (default), the fixed-k baseline on the whole pool "
+                         "(every drawn prompt gets its k rollouts at once), or SARA with the "
+                         "posterior-sampling queue priority")
+    ap.add_argument("--top-p", type=float, default=1.0,
+                    help="nucleus sampling mass (default 1: the full softmax, as every workload uses)")
     ap.add_argument("--graph-iters", type=int, default=16)
     ap.add_argument("--chunk-iters", type=int, default=2048)
     ap.add_argument("--profile-every", type=int, default=16)
@@ -128,6 +134,12 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a HIP device"
     torch.cuda.set_device(0)
     cfg = W.get_config(args.config)
+    if args.mode == "fixed_k":
+        cfg = W.fixed_k_variant(cfg)
+    elif args.mode == "sara_thompson":
+        cfg["alloc"]["mode"] = "sara_thompson"
+    if args.top_p != 1.0:
+        cfg["alloc"]["top_p"] = args.top_p
     t0 = time.time()
     weights = W.make_weights(cfg)
     t_w = time.time() - t0

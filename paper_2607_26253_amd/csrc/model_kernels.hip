@@ -2185,7 +2185,7 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
                            (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, (const float*)lg_out, c->V, 1,
                            (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, 1.0f, c->samp_best,
                            c->samp_idx, 1);
-        PROF_E(c, kPSampleP, c->V, 0);
+        PROF_E(c, kPSampleTopP, c->V, 0);
         nchunks = 1;
       }
     } else {
@@ -2196,6 +2196,7 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
       gemm(c, c->x, c->lm_head, c->rows_M, S, c->V, c->d, sp, 1);
       PROF_E(c, kPGemmLM, c->V, c->d);
       PROF_B(c);
+      const int scls = c->topp ? kPSampleTopP : kPSampleP;
       if (c->topp) {
         launch_k(c, st, k_sample_topp, dim3(std::min(S, 1024)), dim3(kTopPThreads), 0, c->rows_M,
                            (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, (const float*)c->ws, c->V, 0,
@@ -2207,7 +2208,7 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
                            c->rows_M, (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, c->ws, c->V,
                            (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, c->samp_best, c->samp_idx);
       }
-      PROF_E(c, kPSampleP, c->V, 0);
+      PROF_E(c, scls, c->V, 0);
       if (logits) {
         PROF_B(c);
         launch_k(c, st, k_copy_logits, dim3(64, S), dim3(256), 0, c->ctl, c->rows, c->ws, c->V,

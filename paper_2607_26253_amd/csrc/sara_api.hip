@@ -37,6 +37,7 @@ const char* const kProfNames[kPNumClasses] = {
     "k_gemm_bf16_lds<1,8,64,0,0>", "k_gemm_bf16_lds<2,8,64,1,0>", "k_gemm_bf16_lds<2,8,64,2,0>",
     "k_attn_dec<128>", "k_attn_combine", "k_qkv_epilogue", "k_residual_norm_v", "k_swiglu",
     "k_embed_norm", "k_sample_partial", "k_sample_final", "k_decode_rows", "k_copy_logits", "k_qkv_rope",
+    "k_sample_topp",
     ".gemm[q|k|v]", ".gemm[o]", ".gemm[gate|up]", ".gemm[down]", ".gemm[lm_head]"};
 
 // prof_begin reserves an event pair for the next kernel launch; launch_k
@@ -93,6 +94,7 @@ int prof_collect(sara_ctx* c) {
       case kPSwiglu: by = m * N * (8.0 + E); break;
       case kPEmbed: by = m * N * (2.0 * E + 4.0); break;
       case kPSampleP: by = m * N * 4.0; break;
+      case kPSampleTopP: by = m * N * 4.0; break;   // the row's fp32 logits, once
       case kPCopy: by = m * N * 8.0; break;
       default: by = m * 64.0; break;
     }

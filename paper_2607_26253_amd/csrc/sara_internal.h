@@ -195,7 +195,7 @@ namespace sara {
 // one class per kernel (per template instance for the GEMMs, as a kernel
 // trace names them), then a breakdown of the GEMMs by weight matrix
 enum ProfClass { kPGemmN1, kPGemmGU, kPGemmLM, kPAttn, kPCombine, kPQkv, kPResNorm, kPSwiglu,
-                 kPEmbed, kPSampleP, kPSampleF, kPRows, kPCopy, kPQkvRope,
+                 kPEmbed, kPSampleP, kPSampleF, kPRows, kPCopy, kPQkvRope, kPSampleTopP,
                  kPGemmQkv, kPGemmO, kPGemmGu, kPGemmD, kPGemmLm, kPNumClasses };
 extern const char* const kProfNames[kPNumClasses];
 void prof_begin(sara_ctx* c);
