@@ -1547,11 +1547,22 @@ __global__ __launch_bounds__(HD) void k_attn_combine(const int32_t* __restrict__
 // ---------------------------------------------------------------------------
 // (score definition and helpers: see "Gumbel-max sampling helpers")
 
+// top-p helpers: order-preserving key of z (larger z, larger key) and the
+// integer weight of z under the row maximum (see the top-p sampler below)
+__device__ __forceinline__ uint32_t zkey(float z) {
+  uint32_t u = __float_as_uint(z);
+  if ((u & 0x7FFFFFFFu) == 0u) u = 0u;   // -0 and +0 are one value
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ uint64_t nucleus_weight(float z, float zmax) {
+  return (uint64_t)floor(ldexp(exp((double)z - (double)zmax), 44));
+}
+
 __global__ __launch_bounds__(256) void k_sample_partial(const int32_t* __restrict__ M_ptr,
     const int32_t* __restrict__ rid_arr, const int32_t* __restrict__ pos_arr,
-    const RowDesc* __restrict__ rows, const float* __restrict__ logits, int V,
-    const CtlParams* __restrict__ cpd, uint64_t seed, int32_t step, float temp,
-    float* __restrict__ best, int32_t* __restrict__ bidx) {
+    const RowDesc* __restrict__ rows, const float* __restrict__ logits, int V, int by_slot,
+    const uint32_t* __restrict__ thr, const CtlParams* __restrict__ cpd, uint64_t seed, int32_t step,
+    float temp, float* __restrict__ best, int32_t* __restrict__ bidx) {
   __shared__ float sb[256];
   __shared__ int si[256];
   // persistent over (row, vocabulary chunk) items of the live rows
@@ -1566,19 +1577,27 @@ __global__ __launch_bounds__(256) void k_sample_partial(const int32_t* __restric
   const int nblk = (V + 3) >> 2;
   const int per = (nblk + kSampleChunks - 1) / kSampleChunks;
   const int b0 = c * per, b1 = min(nblk, b0 + per);
-  const float* lg = logits + (size_t)i * V;
+  const float* lg = logits + (size_t)(by_slot ? rows[i].slot : i) * V;
+  // top-p: only ids whose key reaches the nucleus threshold take part
+  const uint32_t kth = thr ? thr[i] : 0u;
   float bs = -INFINITY;
   int bi = 0x7FFFFFFF;
   for (int b = b0 + threadIdx.x; b < b1; b += 256) {
+    float z[4];
+    bool any = false;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int v = 4 * b + e;
+      z[e] = (v < V) ? ((temp == 1.0f) ? lg[v] : __fdiv_rn(lg[v], temp)) : -INFINITY;
+      any |= (v < V) && zkey(z[e]) >= kth;
+    }
+    if (!any) continue;
     U32x4 w = philox4x32_10((uint32_t)rid, (uint32_t)gen, (uint32_t)b, 0u, k0, k1);
     uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      int v = 4 * b + e;
-      if (v < V) {
-        float s = __fadd_rn(__fdiv_rn(lg[v], temp), gumbel_exact(ws[e]));
-        better(bs, bi, s, v);
-      }
+      const int v = 4 * b + e;
+      if (v < V && zkey(z[e]) >= kth) better(bs, bi, __fadd_rn(z[e], gumbel_exact(ws[e])), v);
     }
   }
   sb[threadIdx.x] = bs;
@@ -1604,154 +1623,199 @@ __global__ __launch_bounds__(256) void k_sample_partial(const int32_t* __restric
 }
 
 // ---------------------------------------------------------------------------
-// top-p (nucleus) sampler, top_p < 1 (nucleus sampling, Holtzman et al.):
-// one 1024-thread block per row over its fp32 logits.  Mass is counted in
-// integer weights q_v = floor(exp(z_v - z_max) * 2^44), z_v = fp32(logit_v /
-// T), so the cut is an exact integer decision whatever the order of the
-// sums: the nucleus is {v : z_v >= z*}, with z* the largest z whose upper set
-// holds weight >= t = ceil(top_p * Q), Q the total weight; every id tied with
-// the cut is kept.  z* comes from a three-pass radix descent over the
-// order-preserving bits of z (11, 11 and 10 bits) with integer histograms in
-// LDS; the draw is then the Gumbel-max of the full sampler restricted to the
-// nucleus (lowest id on ties).  The row's logits (4 B per id) are read five
-// times, from L2 after the first pass.
+// top-p (nucleus) sampler, top_p < 1 (nucleus sampling, Holtzman et al.),
+// over each row's fp32 logits.  Mass is counted in integer weights
+// q_v = floor(exp(z_v - z_max) * 2^44), z_v = fp32(logit_v / T), so the cut
+// is an exact integer decision whatever the order of the sums: the nucleus
+// is {v : z_v >= z*}, with z* the largest z whose upper set holds weight
+// >= t = ceil(top_p * Q), Q the total weight; every id tied with the cut is
+// kept.  z* comes from a radix descent over the order-preserving bits of z
+// (digits of 11, 11 and 10 bits), each digit in two launches:
+//   k_topp_hist  (row, chunk) blocks: histogram of the weights of the keys
+//                that match the bits decided so far, by the next digit
+//                (2048 bins per chunk, integer LDS atomics: exact)
+//   k_topp_pick  one block per row: sums the chunk histograms in chunk order
+//                and picks the one bin where the weight of the keys above it
+//                and in it first reaches t (after the first digit, with the
+//                weight above the current range carried per row)
+// after k_topp_max has taken the chunk maxima of z.  The Gumbel-max over the
+// nucleus is then k_sample_partial with z*'s key as a threshold.
 // ---------------------------------------------------------------------------
 constexpr int kTopPThreads = 1024;
 constexpr int kTopPWaves = kTopPThreads / 64;
-constexpr int kTopPBins = 2048;
+static_assert(kTopPBins == 2 * kTopPThreads, "two histogram bins per pick thread");
 
-__device__ __forceinline__ uint32_t zkey(float z) {
-  uint32_t u = __float_as_uint(z);
-  if ((u & 0x7FFFFFFFu) == 0u) u = 0u;   // -0 and +0 are one value
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-__device__ __forceinline__ uint64_t nucleus_weight(float z, float zmax) {
-  return (uint64_t)floor(ldexp(exp((double)z - (double)zmax), 44));
+// z = fp32(logit / T); dividing by 1 is exact, so it is skipped
+__device__ __forceinline__ float zval(const float* lg, int v, float temp) {
+  return (temp == 1.0f) ? lg[v] : __fdiv_rn(lg[v], temp);
 }
 
-__global__ __launch_bounds__(kTopPThreads) void k_sample_topp(const int32_t* __restrict__ M_ptr,
-    const int32_t* __restrict__ rid_arr, const int32_t* __restrict__ pos_arr,
+// Vocabulary chunk c of a row for the top-p passes: [c*per, min(V, (c+1)*per))
+// with per a multiple of 4, so a chunk of a row whose length V is a multiple
+// of 4 starts 16-byte aligned.
+__device__ __forceinline__ int topp_chunk_len(int V) { return (((V + kTopPChunks - 1) / kTopPChunks) + 3) & ~3; }
+
+// Calls f(v, z) for every id v of [v0, v1) of the row lg, z = fp32(lg[v] / T).
+// A row that starts 16-byte aligned and whose length is divisible by 4 is
+// read as float4 with kTopPLoads loads of a thread in flight at once (a
+// chunk is ~40 floats per thread, so one or two rounds of loads); any other
+// row one float at a time.
+constexpr int kTopPLoads = 8;
+template <typename F>
+__device__ __forceinline__ void topp_visit(const float* __restrict__ lg, int V, int v0, int v1, float temp, F f) {
+  if ((V & 3) == 0 && (reinterpret_cast<uintptr_t>(lg) & 15) == 0) {
+    const float4* l4 = reinterpret_cast<const float4*>(lg);
+    const int q0 = v0 >> 2, q1 = v1 >> 2;
+    for (int base = q0 + (int)threadIdx.x; base < q1; base += 256 * kTopPLoads) {
+      float4 x[kTopPLoads];
+#pragma unroll
+      for (int u = 0; u < kTopPLoads; ++u) {
+        const int qq = base + u * 256;
+        if (qq < q1) x[u] = l4[qq];
+      }
+#pragma unroll
+      for (int u = 0; u < kTopPLoads; ++u) {
+        const int qq = base + u * 256;
+        if (qq < q1) {
+          const float e4[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) f(4 * qq + e, (temp == 1.0f) ? e4[e] : __fdiv_rn(e4[e], temp));
+        }
+      }
+    }
+  } else {
+    for (int v = v0 + (int)threadIdx.x; v < v1; v += 256) f(v, zval(lg, v, temp));
+  }
+}
+
+__global__ __launch_bounds__(256) void k_topp_max(const int32_t* __restrict__ M_ptr,
     const RowDesc* __restrict__ rows, const float* __restrict__ logits, int V, int by_slot,
-    const CtlParams* __restrict__ cpd, uint64_t seed, int32_t step, float temp, float top_p,
-    float* __restrict__ best, int32_t* __restrict__ bidx, int rstride) {
-  __shared__ unsigned long long hist[kTopPBins];
+    const CtlParams* __restrict__ cpd, float temp, float* __restrict__ pmax) {
+  __shared__ float red[4];
+  if (cpd) temp = cpd->temperature;
+  const int M = *M_ptr;
+  const int per = topp_chunk_len(V);
+  for (int item = blockIdx.x; item < M * kTopPChunks; item += gridDim.x) {
+    const int i = item / kTopPChunks, c = item - i * kTopPChunks;
+    const float* lg = logits + (size_t)(by_slot ? rows[i].slot : i) * V;
+    const int v0 = min(V, c * per), v1 = min(V, v0 + per);
+    float zm = -INFINITY;
+    topp_visit(lg, V, v0, v1, temp, [&](int, float z) { zm = fmaxf(zm, z); });
+    zm = wave_max(zm);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = zm;
+    __syncthreads();
+    if (threadIdx.x == 0) pmax[item] = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    __syncthreads();   // red is reused by the next item
+  }
+}
+
+__device__ __forceinline__ float row_zmax(const float* __restrict__ pmax, int i) {
+  float zm = pmax[(size_t)i * kTopPChunks];
+#pragma unroll
+  for (int c = 1; c < kTopPChunks; ++c) zm = fmaxf(zm, pmax[(size_t)i * kTopPChunks + c]);
+  return zm;
+}
+
+// digit d of the descent: bits 31..21 (d = 0), 20..10 (d = 1), 9..0 (d = 2)
+__device__ __forceinline__ int digit_shift(int d) { return d == 0 ? 21 : (d == 1 ? 10 : 0); }
+
+__global__ __launch_bounds__(256) void k_topp_hist(const int32_t* __restrict__ M_ptr,
+    const RowDesc* __restrict__ rows, const float* __restrict__ logits, int V, int by_slot,
+    const CtlParams* __restrict__ cpd, float temp, const float* __restrict__ pmax, int d,
+    const uint32_t* __restrict__ prefix, unsigned long long* __restrict__ hist) {
+  __shared__ unsigned long long h[kTopPBins];
+  if (cpd) temp = cpd->temperature;
+  const int M = *M_ptr;
+  const int per = topp_chunk_len(V);
+  const int sh = digit_shift(d);
+  const uint32_t dmask = (d == 2) ? 1023u : 2047u;
+  const int hi = (d == 1) ? 21 : 10;   // the bits decided before digit d (d > 0)
+  for (int item = blockIdx.x; item < M * kTopPChunks; item += gridDim.x) {
+    const int i = item / kTopPChunks, c = item - i * kTopPChunks;
+    const float* lg = logits + (size_t)(by_slot ? rows[i].slot : i) * V;
+    const int v0 = min(V, c * per), v1 = min(V, v0 + per);
+    const float zm = row_zmax(pmax, i);
+    const uint32_t pre = (d > 0) ? prefix[i] : 0u;
+    for (int b = threadIdx.x; b < kTopPBins; b += 256) h[b] = 0ull;
+    __syncthreads();
+    topp_visit(lg, V, v0, v1, temp, [&](int, float z) {
+      const uint32_t key = zkey(z);
+      if (d == 0 || (key >> hi) == (pre >> hi)) {
+        const uint64_t q = nucleus_weight(z, zm);
+        if (q) atomicAdd(&h[(key >> sh) & dmask], (unsigned long long)q);
+      }
+    });
+    __syncthreads();
+    unsigned long long* out = hist + (size_t)item * kTopPBins;
+    for (int b = threadIdx.x; b < kTopPBins; b += 256) out[b] = h[b];
+    __syncthreads();   // h is cleared for the next item
+  }
+}
+
+// Per-row state of the descent: prefix (z*'s key bits decided so far; after
+// digit 2, z*'s key), above (weight of keys above the current range), target.
+__global__ __launch_bounds__(kTopPThreads) void k_topp_pick(const int32_t* __restrict__ M_ptr,
+    const CtlParams* __restrict__ cpd, float top_p, int d, const unsigned long long* __restrict__ hist,
+    uint32_t* __restrict__ prefix, unsigned long long* __restrict__ above_arr,
+    unsigned long long* __restrict__ target_arr) {
   __shared__ unsigned long long wsum[kTopPWaves];
-  __shared__ float wmax[kTopPWaves];
-  __shared__ int widx[kTopPWaves];
   __shared__ unsigned long long sel_above, target;
   __shared__ uint32_t sel_digit;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if (cpd) { seed = cpd->seed; step = cpd->step; temp = cpd->temperature; top_p = cpd->top_p; }
-  uint32_t k0, k1;
-  sampler_key(seed, step, k0, k1);
+  if (cpd) top_p = cpd->top_p;
   const int M = *M_ptr;
+  const int sh = digit_shift(d);
   for (int i = blockIdx.x; i < M; i += gridDim.x) {
-    const int rid = rows ? rows[i].rid : rid_arr[i];
-    const int gen = rows ? rows[i].gen : pos_arr[i];
-    const float* lg = logits + (size_t)(by_slot ? rows[i].slot : i) * V;
-    // z_max
-    float zm = -INFINITY;
-    for (int v = tid; v < V; v += kTopPThreads) zm = fmaxf(zm, __fdiv_rn(lg[v], temp));
-    zm = wave_max(zm);
-    if (lane == 0) wmax[wave] = zm;
-    __syncthreads();
-    zm = wmax[0];
+    // the chunk histograms, summed in chunk order
+    const unsigned long long* hr = hist + (size_t)i * kTopPChunks * kTopPBins;
+    unsigned long long h0 = 0ull, h1 = 0ull;
+    for (int c = 0; c < kTopPChunks; ++c) {
+      h0 += hr[(size_t)c * kTopPBins + 2 * tid];
+      h1 += hr[(size_t)c * kTopPBins + 2 * tid + 1];
+    }
+    unsigned long long above = 0ull;
+    uint32_t pre = 0u;
+    if (d == 0) {
+      // the first digit's histograms cover every weight: Q and the target
+      unsigned long long tot = h0 + h1;
 #pragma unroll
-    for (int w = 1; w < kTopPWaves; ++w) zm = fmaxf(zm, wmax[w]);
-    // radix descent: prefix holds the bits of z*'s key decided so far
-    uint32_t prefix = 0u;
-    unsigned long long above = 0ull;   // weight of keys above the current range
-#pragma unroll 1
-    for (int pass = 0; pass < 3; ++pass) {
-      const int sh = (pass == 0) ? 21 : (pass == 1 ? 10 : 0);
-      const uint32_t dmask = (pass == 2) ? 1023u : 2047u;
-      hist[2 * tid] = 0ull;
-      hist[2 * tid + 1] = 0ull;
+      for (int o = 32; o > 0; o >>= 1) tot += __shfl_xor(tot, o, 64);
+      if (lane == 0) wsum[wave] = tot;
       __syncthreads();
-      unsigned long long tot = 0ull;
-      for (int v = tid; v < V; v += kTopPThreads) {
-        const float z = __fdiv_rn(lg[v], temp);
-        const uint32_t key = zkey(z);
-        // the bits decided so far: 31..21 after pass 0, 31..10 after pass 1
-        const int hi = (pass == 1) ? 21 : 10;
-        const bool in = (pass == 0) || ((key >> hi) == (prefix >> hi));
-        if (in) {
-          const uint64_t q = nucleus_weight(z, zm);
-          tot += q;
-          if (q) atomicAdd(&hist[(key >> sh) & dmask], (unsigned long long)q);
-        }
-      }
-      if (pass == 0) {
-        // total weight and target t = ceil(top_p * Q)
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) tot += __shfl_xor(tot, o, 64);
-        if (lane == 0) wsum[wave] = tot;
-      }
-      __syncthreads();
-      if (pass == 0 && tid == 0) {
+      if (tid == 0) {
         unsigned long long Q = 0ull;
         for (int w = 0; w < kTopPWaves; ++w) Q += wsum[w];
         target = (unsigned long long)ceil((double)top_p * (double)Q);
       }
-      // suffix sums of the histogram: thread t owns bins 2t and 2t+1
-      const unsigned long long h0 = hist[2 * tid], h1 = hist[2 * tid + 1];
-      unsigned long long incl = h0 + h1;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const unsigned long long y = __shfl_down(incl, o, 64);
-        if (lane + o < 64) incl += y;
-      }
-      __syncthreads();
-      if (lane == 0) wsum[wave] = incl;
-      __syncthreads();
-      unsigned long long excl = incl - (h0 + h1);
-      for (int w = wave + 1; w < kTopPWaves; ++w) excl += wsum[w];
-      // the one bin where the upper-set weight first reaches the target
-      const unsigned long long t = target;
-      const unsigned long long a1 = above + excl, a0 = a1 + h1;
-      if (a1 < t && a1 + h1 >= t) { sel_digit = 2 * tid + 1; sel_above = a1; }
-      if (a0 < t && a0 + h0 >= t) { sel_digit = 2 * tid; sel_above = a0; }
-      __syncthreads();
-      prefix |= sel_digit << sh;
-      above = sel_above;
-      __syncthreads();   // hist, wsum and the selection are rewritten next pass
+    } else {
+      if (tid == 0) target = target_arr[i];
+      above = above_arr[i];
+      pre = prefix[i];
     }
-    // Gumbel-max over the nucleus {key >= prefix}
-    float bs = -INFINITY;
-    int bi = 0x7FFFFFFF;
-    const int nblk = (V + 3) >> 2;
-    for (int b = tid; b < nblk; b += kTopPThreads) {
-      float z[4];
-      bool any = false;
+    // suffix sums of the histogram: thread t owns bins 2t and 2t+1
+    unsigned long long incl = h0 + h1;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int v = 4 * b + e;
-        z[e] = (v < V) ? __fdiv_rn(lg[v], temp) : -INFINITY;
-        any |= (v < V) && zkey(z[e]) >= prefix;
-      }
-      if (!any) continue;
-      U32x4 w = philox4x32_10((uint32_t)rid, (uint32_t)gen, (uint32_t)b, 0u, k0, k1);
-      const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int v = 4 * b + e;
-        if (v < V && zkey(z[e]) >= prefix) better(bs, bi, __fadd_rn(z[e], gumbel_exact(ws[e])), v);
-      }
+    for (int o = 1; o < 64; o <<= 1) {
+      const unsigned long long y = __shfl_down(incl, o, 64);
+      if (lane + o < 64) incl += y;
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const float s2 = __shfl_xor(bs, o, 64);
-      const int i2 = __shfl_xor(bi, o, 64);
-      better(bs, bi, s2, i2);
-    }
-    if (lane == 0) { wmax[wave] = bs; widx[wave] = bi; }
+    __syncthreads();
+    if (lane == 0) wsum[wave] = incl;
+    __syncthreads();
+    unsigned long long excl = incl - (h0 + h1);
+    for (int w = wave + 1; w < kTopPWaves; ++w) excl += wsum[w];
+    // the one bin where the upper-set weight first reaches the target
+    const unsigned long long t = target;
+    const unsigned long long a1 = above + excl, a0 = a1 + h1;
+    if (a1 < t && a1 + h1 >= t) { sel_digit = 2 * tid + 1; sel_above = a1; }
+    if (a0 < t && a0 + h0 >= t) { sel_digit = 2 * tid; sel_above = a0; }
     __syncthreads();
     if (tid == 0) {
-      for (int w = 1; w < kTopPWaves; ++w) better(bs, bi, wmax[w], widx[w]);
-      best[(size_t)i * rstride] = bs;
-      bidx[(size_t)i * rstride] = bi;
+      prefix[i] = pre | (sel_digit << sh);
+      above_arr[i] = sel_above;
+      if (d == 0) target_arr[i] = t;
     }
-    __syncthreads();   // wmax/widx are reused by the next row
+    __syncthreads();   // wsum, target and the selection are rewritten for the next row
   }
 }
 
@@ -2143,6 +2207,35 @@ int launch_prefill(sara_ctx* c) {
   return SARA_OK;
 }
 
+// Top-p passes over the live rows' logits (lg: [slot][V] when by_slot, else
+// [row][V]) -> z*'s key per row, then the Gumbel-max over the nucleus by
+// k_sample_partial with that threshold: winners [row][kSampleChunks].
+static void launch_topp_decode(sara_ctx* c, hipStream_t st, const float* lg, int by_slot) {
+  const int S = c->S;
+  const CtlParams* cp = (const CtlParams*)c->cp_dev;
+  const int32_t* Mp = c->rows_M;
+  const RowDesc* rw = c->rows;
+  const int g = std::min(S * kTopPChunks, 2048);
+  PROF_B(c);
+  launch_k(c, st, k_topp_max, dim3(g), dim3(256), 0, Mp, rw, lg, c->V, by_slot, cp, 1.0f, c->topp_max);
+  PROF_E(c, kPToppMax, c->V, 0);
+  for (int d = 0; d < 3; ++d) {
+    PROF_B(c);
+    launch_k(c, st, k_topp_hist, dim3(g), dim3(256), 0, Mp, rw, lg, c->V, by_slot, cp, 1.0f,
+             (const float*)c->topp_max, d, (const uint32_t*)c->topp_thr, c->topp_hist);
+    PROF_E(c, kPToppHist, c->V, 0);
+    PROF_B(c);
+    launch_k(c, st, k_topp_pick, dim3(std::min(S, 1024)), dim3(kTopPThreads), 0, Mp, cp, 1.0f, d,
+             (const unsigned long long*)c->topp_hist, c->topp_thr, c->topp_above, c->topp_target);
+    PROF_E(c, kPToppSel, 0, 0);
+  }
+  PROF_B(c);
+  launch_k(c, st, k_sample_partial, dim3(std::min(S * kSampleChunks, 2048)), dim3(256), 0, Mp,
+           (const int32_t*)nullptr, (const int32_t*)nullptr, rw, lg, c->V, by_slot, (const uint32_t*)c->topp_thr, cp,
+           (uint64_t)0, 0, 1.0f, c->samp_best, c->samp_idx);
+  PROF_E(c, kPSampleP, c->V, 0);
+}
+
 int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_free) {
   hipStream_t st = c->stream;
   const int S = c->S;
@@ -2180,13 +2273,8 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
                          SampleArgs{c->rows, (const CtlParams*)c->cp_dev, lg_out, c->samp_best, c->samp_idx, S});
       PROF_E(c, kPGemmLM, c->V, c->d);
       if (c->topp) {
-        PROF_B(c);
-        launch_k(c, st, k_sample_topp, dim3(std::min(S, 1024)), dim3(kTopPThreads), 0, c->rows_M,
-                           (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, (const float*)lg_out, c->V, 1,
-                           (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, 1.0f, c->samp_best,
-                           c->samp_idx, 1);
-        PROF_E(c, kPSampleTopP, c->V, 0);
-        nchunks = 1;
+        launch_topp_decode(c, st, lg_out, 1);
+        nchunks = kSampleChunks;
       }
     } else {
       layers<float>(c, c->rows_M, S, true);
@@ -2195,20 +2283,16 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
       PROF_B(c);
       gemm(c, c->x, c->lm_head, c->rows_M, S, c->V, c->d, sp, 1);
       PROF_E(c, kPGemmLM, c->V, c->d);
-      PROF_B(c);
-      const int scls = c->topp ? kPSampleTopP : kPSampleP;
       if (c->topp) {
-        launch_k(c, st, k_sample_topp, dim3(std::min(S, 1024)), dim3(kTopPThreads), 0, c->rows_M,
-                           (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, (const float*)c->ws, c->V, 0,
-                           (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, 1.0f, c->samp_best,
-                           c->samp_idx, 1);
-        nchunks = 1;
+        launch_topp_decode(c, st, c->ws, 0);
       } else {
+        PROF_B(c);
         launch_k(c, st, k_sample_partial, dim3(std::min(S * kSampleChunks, 2048)), dim3(256), 0,
-                           c->rows_M, (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, c->ws, c->V,
-                           (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f, c->samp_best, c->samp_idx);
+                           c->rows_M, (const int32_t*)nullptr, (const int32_t*)nullptr, c->rows, c->ws, c->V, 0,
+                           (const uint32_t*)nullptr, (const CtlParams*)c->cp_dev, (uint64_t)0, 0, 1.0f,
+                           c->samp_best, c->samp_idx);
+        PROF_E(c, kPSampleP, c->V, 0);
       }
-      PROF_E(c, scls, c->V, 0);
       if (logits) {
         PROF_B(c);
         launch_k(c, st, k_copy_logits, dim3(64, S), dim3(256), 0, c->ctl, c->rows, c->ws, c->V,
@@ -2218,8 +2302,8 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
     }
   }
   PROF_B(c);
-  // chunk winners: [row][kSampleChunks] from k_sample_partial, [chunk][S] from the fused LM head
-  // (one winner per row, at [row], from the nucleus sampler)
+  // chunk winners: [row][kSampleChunks] from k_sample_partial (also after
+  // the top-p passes), [chunk][S] from the fused LM head
   const bool fused = !model_free && c->md.dtype == SARA_BF16 && !c->topp;
   launch_k(c, st, k_sample_final, dim3(std::min(S, 1024)), dim3(256), 0, c->ctl, c->rows,
                      c->samp_best, c->samp_idx, nchunks, fused ? S : 1, fused ? 1 : nchunks, forced, c->flen,
@@ -2245,17 +2329,42 @@ int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* ri
   e = hipMemcpyAsync(mdev, &n_rows, sizeof(int32_t), hipMemcpyHostToDevice, st);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
   const bool topp = top_p < 1.0f;
-  if (topp)
-    hipLaunchKernelGGL(k_sample_topp, dim3(std::min(n_rows, 1024)), dim3(kTopPThreads), 0, st, mdev, rid, pos,
-                       (const RowDesc*)nullptr, logits, V, 0, (const CtlParams*)nullptr, seed, step, temp,
-                       top_p, best, bidx, 1);
-  else
-    hipLaunchKernelGGL(k_sample_partial, dim3(std::min(n_rows * kSampleChunks, 2048)), dim3(256), 0, st, mdev,
-                       rid, pos,
-                       (const RowDesc*)nullptr, logits, V, (const CtlParams*)nullptr, seed, step, temp,
-                       best, bidx);
+  float* pmax = nullptr;
+  unsigned long long* hist = nullptr;
+  unsigned long long* state = nullptr;   // per row: above, target
+  uint32_t* thr = nullptr;
+  if (topp) {
+    e = hipMallocAsync((void**)&pmax, sizeof(float) * (size_t)n_rows * kTopPChunks, st);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
+    e = hipMallocAsync((void**)&hist, sizeof(unsigned long long) * (size_t)n_rows * kTopPChunks * kTopPBins, st);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
+    e = hipMallocAsync((void**)&state, sizeof(unsigned long long) * 2 * (size_t)n_rows, st);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
+    e = hipMallocAsync((void**)&thr, sizeof(uint32_t) * (size_t)n_rows, st);
+    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
+    const int g = std::min(n_rows * kTopPChunks, 2048);
+    hipLaunchKernelGGL(k_topp_max, dim3(g), dim3(256), 0, st, (const int32_t*)mdev, (const RowDesc*)nullptr,
+                       logits, V, 0, (const CtlParams*)nullptr, temp, pmax);
+    for (int d = 0; d < 3; ++d) {
+      hipLaunchKernelGGL(k_topp_hist, dim3(g), dim3(256), 0, st, (const int32_t*)mdev, (const RowDesc*)nullptr,
+                         logits, V, 0, (const CtlParams*)nullptr, temp, (const float*)pmax, d,
+                         (const uint32_t*)thr, hist);
+      hipLaunchKernelGGL(k_topp_pick, dim3(std::min(n_rows, 1024)), dim3(kTopPThreads), 0, st,
+                         (const int32_t*)mdev, (const CtlParams*)nullptr, top_p, d,
+                         (const unsigned long long*)hist, thr, state, state + n_rows);
+    }
+  }
+  hipLaunchKernelGGL(k_sample_partial, dim3(std::min(n_rows * kSampleChunks, 2048)), dim3(256), 0, st, mdev,
+                     rid, pos, (const RowDesc*)nullptr, logits, V, 0, (const uint32_t*)thr,
+                     (const CtlParams*)nullptr, seed, step, temp, best, bidx);
   hipLaunchKernelGGL(k_sample_rows_final, dim3((n_rows + 255) / 256), dim3(256), 0, st, n_rows, rid,
-                     pos, best, bidx, topp ? 1 : kSampleChunks, seed, step, eos, feos, tok);
+                     pos, best, bidx, kSampleChunks, seed, step, eos, feos, tok);
+  if (topp) {
+    (void)hipFreeAsync(pmax, st);
+    (void)hipFreeAsync(hist, st);
+    (void)hipFreeAsync(state, st);
+    (void)hipFreeAsync(thr, st);
+  }
   (void)hipFreeAsync(best, st);
   (void)hipFreeAsync(bidx, st);
   (void)hipFreeAsync(mdev, st);

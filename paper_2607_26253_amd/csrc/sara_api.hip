@@ -37,7 +37,7 @@ const char* const kProfNames[kPNumClasses] = {
     "k_gemm_bf16_lds<1,8,64,0,0>", "k_gemm_bf16_lds<2,8,64,1,0>", "k_gemm_bf16_lds<2,8,64,2,0>",
     "k_attn_dec<128>", "k_attn_combine", "k_qkv_epilogue", "k_residual_norm_v", "k_swiglu",
     "k_embed_norm", "k_sample_partial", "k_sample_final", "k_decode_rows", "k_copy_logits", "k_qkv_rope",
-    "k_sample_topp",
+    "k_topp_max", "k_topp_hist", "k_topp_pick",
     ".gemm[q|k|v]", ".gemm[o]", ".gemm[gate|up]", ".gemm[down]", ".gemm[lm_head]"};
 
 // prof_begin reserves an event pair for the next kernel launch; launch_k
@@ -94,7 +94,9 @@ int prof_collect(sara_ctx* c) {
       case kPSwiglu: by = m * N * (8.0 + E); break;
       case kPEmbed: by = m * N * (2.0 * E + 4.0); break;
       case kPSampleP: by = m * N * 4.0; break;
-      case kPSampleTopP: by = m * N * 4.0; break;   // the row's fp32 logits, once
+      case kPToppMax: by = m * N * 4.0; break;   // the row's fp32 logits, once
+      case kPToppHist: by = m * N * 4.0 + m * (double)kTopPChunks * kTopPBins * 8.0; break;
+      case kPToppSel: by = m * (double)kTopPChunks * kTopPBins * 8.0; break;   // the chunk histograms
       case kPCopy: by = m * N * 8.0; break;
       default: by = m * 64.0; break;
     }
@@ -310,6 +312,13 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   c->topp = c->ad.top_p < 1.0f;
   // nucleus sampling reads fp32 logits; the bf16 LM head writes them here
   if (c->topp && c->md.dtype == SARA_BF16) ALLOC(c->topp_logits, sizeof(float) * (size_t)c->S * c->V);
+  if (c->topp) {
+    ALLOC(c->topp_max, sizeof(float) * (size_t)c->S * kTopPChunks);
+    ALLOC(c->topp_hist, sizeof(unsigned long long) * (size_t)c->S * kTopPChunks * kTopPBins);
+    ALLOC(c->topp_thr, sizeof(uint32_t) * (size_t)c->S);
+    ALLOC(c->topp_above, sizeof(unsigned long long) * (size_t)c->S);
+    ALLOC(c->topp_target, sizeof(unsigned long long) * (size_t)c->S);
+  }
   ALLOC(c->g_off, sizeof(int32_t) * (c->U + 1));
   ALLOC(c->g_r, sizeof(float) * nroll);
   ALLOC(c->g_adv, sizeof(float) * nroll);

@@ -22,6 +22,8 @@ constexpr int kDecPages = 4 * kDecPpw;  // KV pages per context split in the dec
 constexpr int kMaxSplitsDec = 12;    // split-K partials of a decode GEMM (summed in one batch; a multiple of 4)
 constexpr int kAttnTile = 64;        // tokens per LDS tile inside a split
 constexpr int kSampleChunks = 16;    // vocabulary chunks per sampled row
+constexpr int kTopPChunks = 16;      // vocabulary chunks per row in the top-p passes
+constexpr int kTopPBins = 2048;      // 11-bit digits of the top-p radix descent
 constexpr int kCtlThreads = 1024;    // threads of the single-workgroup controller
 constexpr int kMaxQueue = 4096;      // pending rollouts held in LDS by the refill
 constexpr int kMaxSlots = 4096;
@@ -157,6 +159,11 @@ struct sara_ctx {
   int32_t* samp_idx = nullptr;
   bool topp = false;              // top_p < 1: nucleus sampler after the LM head
   float* topp_logits = nullptr;   // [S][V] fp32 logits for it (bf16 models)
+  float* topp_max = nullptr;      // [S][kTopPChunks] chunk maxima of z
+  unsigned long long* topp_hist = nullptr;   // [S][kTopPChunks][kTopPBins] chunk weight histograms
+  uint32_t* topp_thr = nullptr;   // [S] key bits of each row's nucleus threshold z* (all of them at the end)
+  unsigned long long* topp_above = nullptr;    // [S] weight above the descent's current range
+  unsigned long long* topp_target = nullptr;   // [S] target weight t
 
   // GRPO of committed groups
   int32_t* g_off = nullptr;
@@ -195,7 +202,7 @@ namespace sara {
 // one class per kernel (per template instance for the GEMMs, as a kernel
 // trace names them), then a breakdown of the GEMMs by weight matrix
 enum ProfClass { kPGemmN1, kPGemmGU, kPGemmLM, kPAttn, kPCombine, kPQkv, kPResNorm, kPSwiglu,
-                 kPEmbed, kPSampleP, kPSampleF, kPRows, kPCopy, kPQkvRope, kPSampleTopP,
+                 kPEmbed, kPSampleP, kPSampleF, kPRows, kPCopy, kPQkvRope, kPToppMax, kPToppHist, kPToppSel,
                  kPGemmQkv, kPGemmO, kPGemmGu, kPGemmD, kPGemmLm, kPNumClasses };
 extern const char* const kProfNames[kPNumClasses];
 void prof_begin(sara_ctx* c);
