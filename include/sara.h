@@ -90,7 +90,7 @@ typedef struct {
  *               id tied at the cut; mass counted in integer weights
  *               floor(exp(z - z_max) * 2^44) of z = fp32(logit / T)).  The
  *               nucleus path writes fp32 logits [n_slots][vocab] (library
- *               memory for bf16 models) and runs a separate sampler kernel
+ *               memory for bf16 models) and runs separate sampler kernels
  *   forced_eos_u32  per-token probability x / 2^32 of a forced EOS (0 = off)
  *   prio_quant_bits  quantisation of the p_eff priority key (1..21)
  *   seed        key material of the counter-based sampler and reward hash
