@@ -1580,25 +1580,52 @@ __global__ __launch_bounds__(256) void k_sample_partial(const int32_t* __restric
   const float* lg = logits + (size_t)(by_slot ? rows[i].slot : i) * V;
   // top-p: only ids whose key reaches the nucleus threshold take part
   const uint32_t kth = thr ? thr[i] : 0u;
-  float bs = -INFINITY;
-  int bi = 0x7FFFFFFF;
+  // Pass 1: fast scores (fp32 noise estimate) and their maximum over the
+  // chunk.  Pass 2: the exact score (fp64 noise) of every id whose fast score
+  // is within the estimate's error bound of that maximum; the chunk's exact
+  // winner is always among them (the bound of the fused LM-head sampler).
+  float fmx = -INFINITY;
   for (int b = b0 + threadIdx.x; b < b1; b += 256) {
     float z[4];
-    bool any = false;
+    bool in[4], any = false;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int v = 4 * b + e;
       z[e] = (v < V) ? ((temp == 1.0f) ? lg[v] : __fdiv_rn(lg[v], temp)) : -INFINITY;
-      any |= (v < V) && zkey(z[e]) >= kth;
+      in[e] = (v < V) && zkey(z[e]) >= kth;
+      any |= in[e];
     }
     if (!any) continue;
     U32x4 w = philox4x32_10((uint32_t)rid, (uint32_t)gen, (uint32_t)b, 0u, k0, k1);
-    uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (in[e]) fmx = fmaxf(fmx, __fadd_rn(z[e], gumbel_fast(ws[e])));
+  }
+  fmx = wave_max(fmx);
+  if ((threadIdx.x & 63) == 0) sb[threadIdx.x >> 6] = fmx;
+  __syncthreads();
+  const float floor_ = gumbel_candidate_floor(fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
+  __syncthreads();   // sb is rewritten below
+  float bs = -INFINITY;
+  int bi = 0x7FFFFFFF;
+  for (int b = b0 + threadIdx.x; b < b1; b += 256) {
+    float z[4];
+    bool in[4], any = false;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const int v = 4 * b + e;
-      if (v < V && zkey(z[e]) >= kth) better(bs, bi, __fadd_rn(z[e], gumbel_exact(ws[e])), v);
+      z[e] = (v < V) ? ((temp == 1.0f) ? lg[v] : __fdiv_rn(lg[v], temp)) : -INFINITY;
+      in[e] = (v < V) && zkey(z[e]) >= kth;
+      any |= in[e];
     }
+    if (!any) continue;
+    U32x4 w = philox4x32_10((uint32_t)rid, (uint32_t)gen, (uint32_t)b, 0u, k0, k1);
+    const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (in[e] && __fadd_rn(z[e], gumbel_fast(ws[e])) >= floor_)
+        better(bs, bi, __fadd_rn(z[e], gumbel_exact(ws[e])), 4 * b + e);
   }
   sb[threadIdx.x] = bs;
   si[threadIdx.x] = bi;
