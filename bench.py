@@ -63,8 +63,10 @@ def describe(cfg):
             f"max_new={a['max_new']} mode={a['mode']}" + (f" top_p={a['top_p']}" if a.get("top_p", 1.0) != 1.0 else ""))
 
 
-def cpu_baseline(cfg, weights, seconds_target=15.0):
-    """Oracle rollout generation rate on a bounded sample, host cores."""
+def cpu_baseline(cfg, weights):
+    """Oracle rollout generation rate on a bounded sample, host cores (about
+    10-15 s on a 16-thread host: prefill of two prompts, then 32 lockstep
+    decode steps of 8 rollouts)."""
     from oracle import run as ORUN
     try:
         from threadpoolctl import threadpool_info
@@ -80,7 +82,7 @@ def cpu_baseline(cfg, weights, seconds_target=15.0):
     for name, _ in W.weight_specs(c["model"]):   # weight conversion outside the timing
         src.dec.w(name)
     t_setup = time.time() - t0
-    prompts, rollouts, new_tokens = 2, 4, 16
+    prompts, rollouts, new_tokens = 2, 4, 32
     a_max = a["max_new"]
     src.a = dict(a, max_new=new_tokens)
     t0 = time.time()
