@@ -212,3 +212,53 @@ def test_top_p_sampling_is_truncated_softmax():
     # top_p = 1 is the plain sampler, token for token
     for rid in range(200):
         assert sampler.sample(logits, T, 9, 0, rid, 4, 1.0)[0] == sampler.sample(logits, T, 9, 0, rid, 4)[0]
+
+
+# --- rollout length distributions --------------------------------------------
+
+def test_forced_eos_lengths_match_the_truncated_geometric():
+    """3B workload: a forced EOS with per-token probability thr / 2^32
+    (thr = floor(2^32 / 800)) ends a rollout at its first firing, else at the
+    2048-token cap.  Closed form: P(capped) = (1 - p)^2048 = 7.73%, mean
+    length (1 - (1 - p)^2048) / p = 738.3."""
+    import workloads as W
+    from oracle.philox import philox4x32
+    cfg = W.get_config("qwen3b_shape")
+    thr, cap = cfg["alloc"]["forced_eos_u32"], cfg["alloc"]["max_new"]
+    assert thr == (1 << 32) // 800 and cap == 2048
+    seed, step = W.sampling_seed(cfg), 0
+    k0, k1 = sampler.key_of(seed, step)
+    R = 3000
+    rid = np.arange(R, dtype=np.uint64)[:, None]
+    pos = np.arange(cap, dtype=np.uint64)[None, :]
+    words = philox4x32(rid, pos, 0, 1, k0, k1)[..., 0]
+    for r, i in [(0, 0), (7, 11), (2999, 2047), (1234, 600)]:
+        assert int(words[r, i]) == sampler.forced_eos_word(seed, step, r, i)
+    fired = words < np.uint32(thr)
+    L = np.where(fired.any(axis=1), fired.argmax(axis=1) + 1, cap).astype(np.float64)
+    p = thr / 2.0 ** 32
+    capped = (1 - p) ** cap
+    mean = (1 - capped) / p
+    assert abs(capped - 0.0773) < 5e-4 and abs(mean - 738.3) < 0.5
+    var = sum((2 * i - 1) * (1 - p) ** (i - 1) for i in range(1, cap + 1)) - mean ** 2
+    assert abs(L.mean() - mean) < 5 * math.sqrt(var / R)
+    assert abs(np.mean(L == cap) - capped) < 5 * math.sqrt(capped * (1 - capped) / R)
+
+
+def test_long_rollout_lengths_match_the_clamped_lognormal():
+    """Long-rollout workload: lengths clamp(round(exp(ln 1200 + 0.6 z)), 1,
+    4096).  Closed forms of the lognormal: E[min(X, c)] = e^(mu + s^2/2)
+    Phi((ln c - mu - s^2) / s) + c P(X >= c) = 1415 and P(X >= 4096) = 2.0%."""
+    import workloads as W
+    cfg = W.get_config("long_ragged_1p5b")
+    L = np.concatenate([W.make_pool(cfg, t)["forced_len"].reshape(-1) for t in range(4)]).astype(np.float64)
+    mu, s, c = math.log(1200.0), 0.6, 4096.0
+    z = (math.log(c) - mu) / s
+    p_cap = stats.norm.sf(z)
+    mean = math.exp(mu + s * s / 2) * stats.norm.cdf(z - s) + c * p_cap
+    assert abs(mean - 1415) < 2 and abs(p_cap - 0.0204) < 5e-4
+    sd = float(np.sqrt(np.mean((np.minimum(np.exp(mu + s * np.random.default_rng(0).standard_normal(200000)), c)
+                                - mean) ** 2)))
+    assert abs(L.mean() - mean) < 5 * sd / math.sqrt(len(L)) + 0.5   # + rounding to integers
+    assert abs(np.mean(L >= c) - p_cap) < 5 * math.sqrt(p_cap * (1 - p_cap) / len(L))
+    assert L.min() >= 1 and L.max() <= c
