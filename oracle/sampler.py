@@ -25,6 +25,13 @@ z_v = fp32(logit_v / T) (+0 for a zero), weight q_v = floor(exp(z_v - z_max)
 q_v, target t = ceil(fp64(top_p) * fp64(Q)); the nucleus is {v : z_v >= z*}
 with z* the largest z value whose set {z_v >= z*} holds weight >= t.
 top_p = 1 keeps the whole vocabulary (no weight is dropped).
+
+Pins (tests): Philox4x32-10 published known-answer vectors; uniformity and
+Gumbel moments; chi-square of the Gumbel-max draw against softmax; the
+nucleus against its prefix definition in 50-digit arithmetic, ties at the
+cut, the greedy and top_p = 1 limits and minimality; chi-square of the top-p
+draw against the renormalised truncated softmax; the forced-EOS frequency
+and the rollout-length law it implies (truncated geometric).
 """
 import math
 
