@@ -207,7 +207,10 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
   c->md = *md;
   c->ad = *ad;
   c->stream = (hipStream_t)stream;
-  HIP_TRY(hipGetDevice(&c->device), "hipGetDevice");
+  {
+    const hipError_t e = hipGetDevice(&c->device);
+    if (e != hipSuccess) { delete c; return hip_fail(e, "hipGetDevice"); }
+  }
   c->L = md->n_layers; c->d = md->d_model; c->hq = md->n_heads; c->hkv = md->n_kv_heads;
   c->hd = md->head_dim; c->ffn = md->d_ffn; c->V = md->vocab; c->G = c->hq / c->hkv;
   c->qdim = c->hq * c->hd; c->nqkv = (c->hq + 2 * c->hkv) * c->hd;
