@@ -6,13 +6,18 @@ active (replayed from a HIP graph), and GRPO advantages of the committed
 groups.  Inputs (weights, prompt pools) are resident in HBM before the timed
 region.  Prints one JSON line.
 
-value  = rollout tokens generated per second over the K timed steps.
-roofline: per-kernel HIP-event timing of one further allocation step run
-eagerly (every `--profile-every`-th decode step profiled); the dominant
-kernel is the class with the largest share of decode time, its achieved
-GB/s is algorithmic bytes / event-timed duration.
+value  = rollout tokens generated per second over the timed steps.  Whole
+allocation steps are timed until --steps are done or --time-budget seconds
+are spent (always at least one); `steps` and `warmup` report the counts
+actually run.
+roofline: one further allocation step replayed from the same graph, with one
+eager iteration after every --profile-chunk loop iterations whose kernels are
+timed from the dispatch's own start/end stamps (HIP events on the library's
+stream); the dominant kernel is the class with the largest summed time, its
+achieved rate is algorithmic bytes (or flops, when its intensity is past the
+ridge point) per launch over its mean duration.
 cpu_baseline: the CPU oracle generating rollouts of the same model shape on a
-bounded sample (one prompt's prefill + a few rollouts x a few tokens).
+bounded sample (two prompts' prefill + a few rollouts x a few tokens).
 """
 import argparse
 import json
@@ -113,7 +118,15 @@ def main():
                     help="nucleus sampling mass (default 1: the full softmax, as every workload uses)")
     ap.add_argument("--graph-iters", type=int, default=16)
     ap.add_argument("--chunk-iters", type=int, default=2048)
-    ap.add_argument("--profile-every", type=int, default=16)
+    ap.add_argument("--time-budget", type=float, default=60.0,
+                    help="wall-clock seconds of timed work: whole allocation steps run until --steps are "
+                         "done or this is spent (at least one); the line reports the steps actually timed")
+    ap.add_argument("--warmup-budget", type=float, default=10.0,
+                    help="further warm-up steps start only within this many seconds (one always runs)")
+    ap.add_argument("--profile-budget", type=float, default=45.0,
+                    help="wall-clock seconds of the kernel-timed pass")
+    ap.add_argument("--profile-chunk", type=int, default=48,
+                    help="graph-replayed loop iterations between two kernel-timed eager iterations")
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--counter-pass", type=int, default=0,
@@ -124,6 +137,8 @@ def main():
                     help="profiling mode: only replay this many decode/decide/refill iterations of "
                          "step 0 from the HIP graph (for kernel traces), then exit")
     args = ap.parse_args()
+    if args.steps < 1 or args.warmup < 0:
+        ap.error("--steps must be >= 1 and --warmup >= 0")
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): the allocation step would "
               f"shard by prompts (a model replica, slot pool and controller per GPU, no traffic "
@@ -197,9 +212,12 @@ def main():
         ctx.close()
         return
 
-    n_total = args.warmup + args.steps + (0 if args.no_profile else 1)
+    # Whole allocation steps run until the requested count is reached or the
+    # step's wall-clock budget is spent (one step of the 1.5B workload takes
+    # tens of seconds); the line reports the counts actually run.
+    n_pools = max(1, args.warmup) + max(1, args.steps) + 1
     pools = []
-    for s in range(n_total):
+    for s in range(n_pools):
         p = W.make_pool(cfg, s)
         d_tok = torch.from_numpy(p["tokens"]).cuda()
         d_p = torch.from_numpy(p["p"]).cuda()
@@ -223,18 +241,25 @@ def main():
         ctx.sara_finish_step(1e-6)
         return ctx.sara_query()
 
-    for i in range(args.warmup):
-        st = one_step(i, f"warmup {i}")
-        print(f"[bench] warmup step {i}: {st['tokens']} tokens, {st['decode_steps']} decode steps",
+    # warm-up: builds and instantiates the decode graph (one step is enough)
+    n_warm, tw = 0, time.perf_counter()
+    while n_warm < args.warmup and (n_warm == 0 or time.perf_counter() - tw < args.warmup_budget):
+        st = one_step(n_warm, f"warmup {n_warm}")
+        print(f"[bench] warmup step {n_warm}: {st['tokens']} tokens, {st['decode_steps']} decode steps",
               file=sys.stderr, flush=True)
+        n_warm += 1
 
     torch.cuda.synchronize()
     stats = []
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        stats.append(one_step(args.warmup + i, f"step {i}"))
+    while len(stats) < args.steps:
+        i = len(stats)
+        stats.append(one_step(n_warm + i, f"step {i}"))
+        if time.perf_counter() - t0 >= args.time_budget:
+            break
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
+    n_steps = len(stats)
     for i, st in enumerate(stats):
         print(f"[bench] step {i}: tokens {st['tokens']} rollouts {st['rollouts']} committed {st['committed']} "
               f"abandoned {st['abandoned']} drawn {st['drawn']} decode steps {st['decode_steps']}",
@@ -246,36 +271,44 @@ def main():
 
     out = {
         "metric": "rollout tokens/s + effective groups/s on 1 GPU; decode HBM GB/s % of peak",
-        "value": tokens / dt, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": 1e3 * dt / args.steps, "higher_is_better": True,
+        "value": tokens / dt, "unit": "tokens/s", "n_gpus": 1, "steps": n_steps,
+        "warmup": n_warm, "ms_per_step": 1e3 * dt / n_steps, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": cfg["model"]["dtype"],
         "data": "synthetic (random-init weights, seeded prompt pools and success rates)",
         "config": {"workload": describe(cfg)},
+        "steps_requested": args.steps, "warmup_requested": args.warmup,
+        "time_budget_s": args.time_budget, "timed_s": dt,
         "effective_groups_per_s": committed / dt,
         "rollouts_per_effective_group": (rollouts / committed) if committed else None,
         "tokens_per_effective_group": (tokens / committed) if committed else None,
         "decode_steps_per_s": decode_steps / dt,
+        "per_step": [{k: s[k] for k in ("tokens", "rollouts", "committed", "abandoned", "drawn", "decode_steps")}
+                     for s in stats],
     }
 
     if not args.no_profile:
-        p, d_tok, d_p, d_fl = pools[-1]
+        # One further allocation step on its own pool, replayed from the same
+        # graph in chunks of --profile-chunk loop iterations, with one eager
+        # iteration after each chunk timed kernel by kernel: the sample spans
+        # the whole step (every occupancy it goes through) at graph speed.
+        p, d_tok, d_p, d_fl = pools[n_warm + n_steps]
         ctx.sara_begin_step(d_tok, p["offsets"], d_p, d_fl, p["step"])
         ctx.sara_reset_profile()
-        it, n_prof = 0, 0
+        it, n_prof, done = 0, 0, False
         tprof = time.perf_counter()
-        while True:
-            if it % 16 == 0 and ctx.sara_query()["done"]:
-                break
-            if it % 2048 == 0:
-                print(f"[bench] profiled pass: {it} decode steps", file=sys.stderr, flush=True)
-            on = (it % args.profile_every) == 0
-            ctx.sara_set_profiling(on)
+        while not done and time.perf_counter() - tprof < args.profile_budget:
+            ctx.sara_set_profiling(True)
             ctx.sara_decode_step(None, None, False)
-            n_prof += int(on)
+            ctx.sara_set_profiling(False)
             ctx.sara_posterior_decide()
             ctx.sara_refill()
             it += 1
-        ctx.sara_set_profiling(False)
+            n_prof += 1
+            it += ctx.sara_run(None, graph_iters=args.graph_iters, max_iters=args.profile_chunk)
+            done = bool(ctx.sara_query()["done"])
+            if n_prof % 64 == 0:
+                print(f"[bench] profiled pass: {it} loop iterations, {n_prof} profiled",
+                      file=sys.stderr, flush=True)
         prof = ctx.sara_read_profile()
         tprof = time.perf_counter() - tprof
         allc = [k for k in prof if k["launches"] > 0]
@@ -285,19 +318,29 @@ def main():
         dom = max(dec, key=lambda k: k["ms"])
         per_launch_ms = dom["ms"] / dom["launches"]
         per_launch_by = dom["bytes"] / dom["launches"]
-        ach = per_launch_by / (per_launch_ms * 1e-3) / 1e9
+        per_launch_fl = dom["flops"] / dom["launches"]
+        ach_gbs = per_launch_by / (per_launch_ms * 1e-3) / 1e9
+        ach_tfs = per_launch_fl / (per_launch_ms * 1e-3) / 1e12
+        # roof from the kernel's arithmetic intensity against the ridge point
+        # (peak flop/s over peak byte/s)
+        ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+        mfma = cfg["model"]["dtype"] == "bf16" and per_launch_by > 0 and per_launch_fl / per_launch_by > ridge
         tr = measured_traffic(dom["name"])
         out["roofline"] = {
-            "kernel": dom["name"], "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": ach / HBM_PEAK_GBS, "traffic": tr["traffic"] if tr else None,
+            "kernel": dom["name"], "bound": "mfma" if mfma else "hbm",
+            "achieved": ach_tfs if mfma else ach_gbs,
+            "peak": BF16_PEAK_TFLOPS if mfma else HBM_PEAK_GBS, "unit": "TFLOP/s" if mfma else "GB/s",
+            "frac": (ach_tfs / BF16_PEAK_TFLOPS) if mfma else (ach_gbs / HBM_PEAK_GBS),
+            "traffic": tr["traffic"] if tr else None,
             "traffic_measured_at": ({k: tr[k] for k in ("regime", "alg_bytes_per_launch", "ratio", "source")}
                                     if tr else None),
             "avg_launch_us": per_launch_ms * 1e3, "alg_bytes_per_launch": per_launch_by,
-            "launches_timed": dom["launches"],
-            "tflops": dom["flops"] / (dom["ms"] * 1e-3) / 1e12 if dom["flops"] else None,
+            "alg_flops_per_launch": per_launch_fl, "intensity_flop_per_byte": per_launch_fl / per_launch_by,
+            "ridge_flop_per_byte": ridge, "launches_timed": dom["launches"],
+            "hbm_gbs": ach_gbs, "tflops": ach_tfs,
         }
         out["decode_profile"] = {
-            "decode_steps_profiled": n_prof, "decode_steps": it,
+            "profiled_iterations": n_prof, "loop_iterations": it, "step_done": done,
             "kernel_time_ms": tot_ms, "alg_bytes": tot_by,
             "decode_hbm_gbs": tot_by / (tot_ms * 1e-3) / 1e9,
             "decode_hbm_frac": tot_by / (tot_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
@@ -307,7 +350,7 @@ def main():
                         for k in allc},
             "wall_s": tprof,
         }
-        print(f"[bench] profiled {n_prof} of {it} decode steps; dominant {dom['name']}: {ach:.0f} GB/s; "
+        print(f"[bench] profiled {n_prof} of {it} loop iterations; dominant {dom['name']}: {ach_gbs:.0f} GB/s; "
               f"decode kernels {out['decode_profile']['decode_hbm_gbs']:.0f} GB/s", file=sys.stderr, flush=True)
 
     if not args.no_cpu_baseline:

@@ -124,7 +124,12 @@ typedef struct {
   int64_t n_decisions, n_draws, n_assigns, n_finishes;  /* log lengths       */
 } sara_step_stats;
 
-/* Create a context on the current HIP device.
+/* Create a context on the current HIP device for one allocation problem:
+ * the inputs of Algorithm 1 (its Require line: pool, target B, group size k,
+ * probe n0, threshold tau_low, prior (alpha0, beta0), budget cap) plus the
+ * defaults of the implementation-details appendix ("Defaults and history
+ * warm-start": commit_min, the 6Bk safety cap) and the decoder that
+ * generates the rollouts.
  * d_weights: n_weights device pointers in this order, each row-major
  * [out][in] in the model dtype (bf16 as raw 16-bit patterns):
  *   embed[V][d]; per layer l: attn_norm[d], wq[Hq*hd][d], wk[Hkv*hd][d],
@@ -138,7 +143,9 @@ int sara_init(const sara_model_desc* model, const sara_alloc_desc* alloc,
               const void* const* d_weights, int32_t n_weights, void* stream,
               sara_ctx** out);
 
-/* Start an allocation step over a pool of pool_U prompts.
+/* Start an allocation step over a pool of pool_U prompts (Algorithm 1, first
+ * state: the collected set empty, B fresh prompts probed with n0 rollouts
+ * each; the pool is the prompt pool D of its Require line).
  * d_tokens: concatenated prompt token ids (device, int32);
  * h_offsets: pool_U + 1 host offsets into d_tokens (prompt u is
  *   [h_offsets[u], h_offsets[u+1]), length 1..max_prompt);
@@ -153,7 +160,11 @@ int sara_init(const sara_model_desc* model, const sara_alloc_desc* alloc,
 int sara_begin_step(sara_ctx* ctx, const int32_t* d_tokens, const int32_t* h_offsets,
                     const double* d_p, const int32_t* d_forced_len, int32_t step_index);
 
-/* One decode step over every occupied slot: embedding, n_layers decoder
+/* One decode step over every occupied slot, one token for each running
+ * rollout: the batched generation call of Algorithm 1 ("one batched call"),
+ * and of the implementation-details appendix ("Round-synchronous batched
+ * scheduling": one generation call over all active prompts), taken here one
+ * token at a time so that decisions can follow every token.  Embedding, n_layers decoder
  * layers over the paged KV cache, LM head, Gumbel-max sampling keyed by
  * (seed, step_index, rollout id uid*k + j, generated index), forced EOS,
  * reward hash, termination.
@@ -165,29 +176,42 @@ int sara_begin_step(sara_ctx* ctx, const int32_t* d_tokens, const int32_t* h_off
 int sara_decode_step(sara_ctx* ctx, const int32_t* d_forced_tok, float* d_logits,
                      int32_t model_free);
 
-/* Apply the finished rollouts of the last decode step to their prompts'
- * (n, s) and decide every quiescent active prompt with Eq. decide:
+/* Section 3.2-3.3 (Beta posterior, Proposition 1, Eq. decide; the loop body
+ * of Algorithm 1).  Apply the finished rollouts of the last decode step to
+ * their prompts' (n, s) and decide every quiescent active prompt with Eq. decide:
  * Beta(alpha0 + s, beta0 + n - s), p_eff by Proposition 1 (fp64 lgamma),
  * commit / abandon (refund k - n) / continue (queue more rollouts). */
 int sara_posterior_decide(sara_ctx* ctx);
 
-/* Draw fresh prompts while |A| < B - |C|, budget_left >= k and the pool is
+/* The reallocation of Algorithm 1 (draw fresh prompts, probe n0, toward the
+ * remaining need; advance continuing prompts prioritised by p_eff, section
+ * 3.3).  Draw fresh prompts while |A| < B - |C|, budget_left >= k and the pool is
  * not exhausted; order the pending rollouts by (quantised p_eff desc, uid,
  * j) and assign them to free slots in ascending slot order. */
 int sara_refill(sara_ctx* ctx);
 
-/* Drive the step to completion: replays [decode, decide, refill] from a HIP
- * graph of graph_iters iterations, polling the done flag asynchronously.
+/* The while loop of Algorithm 1 on the device (implementation-details
+ * appendix, "Round-synchronous batched scheduling": rounds of one batched
+ * generation call followed by the decisions and the reallocation; here the
+ * decisions follow every decode step and no round barrier reaches the
+ * host).  Drives the step to completion: replays [decode, decide, refill]
+ * from a HIP graph of graph_iters iterations, polling the done flag
+ * asynchronously.
  * Synchronises before returning.  d_forced_tok as in sara_decode_step.
  * *iters_out receives the number of loop iterations enqueued. */
 int sara_run(sara_ctx* ctx, const int32_t* d_forced_tok, int32_t graph_iters,
              int64_t max_iters, int64_t* iters_out);
 
-/* Synchronise the stream and report the step's counters. */
+/* Synchronise the stream and report the step's counters: the loop state of
+ * Algorithm 1 (|C|, |A|, budget left) and its cost in rollouts and tokens
+ * (experimental setup appendix, "Metrics").  Returns SARA_EDEVICE when the
+ * device error word is set. */
 int sara_query(sara_ctx* ctx, sara_step_stats* out);
 
-/* Build the CSR of committed groups (ascending uid, rollouts in j order) and
- * compute their GRPO advantages with grpo_group_advantages.  Enqueued. */
+/* Last line of Algorithm 1: the GRPO update (Eq. grpo, section 2) receives
+ * the effective groups of C.  Build the CSR of committed groups (ascending
+ * uid, rollouts in j order) and compute their advantages with
+ * grpo_group_advantages.  Enqueued. */
 int sara_finish_step(sara_ctx* ctx, float eps);
 
 /* History warm start (implementation details, "defaults and history
@@ -222,6 +246,18 @@ int sara_set_warm_start(sara_ctx* ctx, const int32_t* d_ids, double* d_a, double
  * SARA_ESTATE when no warm start is set or no step has begun. */
 int sara_warm_start_update(sara_ctx* ctx, double lambda);
 
+/* Asynchronous poll of the loop condition of Algorithm 1: enqueues on the
+ * context's stream a small kernel that writes the device error word to
+ * h_pinned[1] and then, after a system-scope fence, the done flag (1 once no
+ * prompt is active) to h_pinned[0], and returns at once.  h_pinned: 2 int32
+ * of pinned host memory (hipHostMalloc, or a pinned torch tensor) owned by
+ * the caller.  Set h_pinned[0] = -1 before the call and spin on it (volatile
+ * read) until it changes, or synchronise the stream: h_pinned[1] is valid
+ * once h_pinned[0] has changed, which lets the host overlap its own work with
+ * the decode loop.  Errors: SARA_EINVAL for a null argument or memory that
+ * is not pinned host memory; SARA_ESTATE before sara_begin_step. */
+int sara_poll(sara_ctx* ctx, int32_t* h_pinned);
+
 /* Copy results to host (synchronises).  Any pointer may be NULL.
  *   h_tokens  [pool_U*k][max_new] int32 appended tokens (-1 past the end)
  *   h_sampled [pool_U*k][max_new] int32 sampler choices
@@ -247,12 +283,19 @@ int sara_read_logs(sara_ctx* ctx, int64_t* h_dec, int64_t cap_dec, int64_t* h_dr
 int sara_read_advantages(sara_ctx* ctx, int32_t* h_offsets, float* h_rewards, float* h_adv,
                          int32_t cap);
 
-/* Closed-form predictor of Proposition 1 (Eq. peff) for count prompts:
- * d_out[i] = P(group of size k is mixed | d_n[i] observed, d_s[i] successes)
- * under the prior Beta(alpha0, beta0), fp64 via lgamma.  Pure; enqueued on
- * stream. */
-int sara_peff_batch(const int32_t* d_n, const int32_t* d_s, int32_t k, double alpha0,
-                    double beta0, int32_t count, double* d_out, void* stream);
+/* Closed-form predictor of Proposition 1 (Eq. peff) for count prompts, each
+ * under its own prior (section 3.2; per-prompt priors are what the history
+ * warm start of the implementation-details appendix produces):
+ *   d_out[i] = P(group of size k is mixed | d_n[i] observed, d_s[i]
+ *              successes) under the prior Beta(d_alpha[i], d_beta[i])
+ * in fp64 via lgamma (the posterior is Beta(alpha + s, beta + n - s)).
+ * All five arrays are device memory of count elements, owned by the caller.
+ * Entries with a non-positive or non-finite prior parameter, or outside
+ * 0 <= s <= n <= k, give NaN.  Argument errors (count < 0, k < 1, a null
+ * array with count > 0) return SARA_EINVAL and enqueue nothing.  Pure;
+ * enqueued on stream. */
+int sara_peff_batch(const double* d_alpha, const double* d_beta, const int32_t* d_n,
+                    const int32_t* d_s, int32_t k, int32_t count, double* d_out, void* stream);
 
 /* Group-relative advantages of Eq. grpo: for group g with rewards
  * d_r[d_group_off[g] .. d_group_off[g+1]), A_i = (r_i - mean) / (std + eps),

@@ -25,7 +25,7 @@ EXPORTED = ["sara_init", "sara_begin_step", "sara_decode_step", "sara_posterior_
             "sara_refill", "sara_run", "sara_query", "sara_finish_step", "sara_read_rollouts",
             "sara_read_logs", "sara_read_advantages", "sara_peff_batch", "grpo_group_advantages",
             "sara_sample_logits", "sara_gumbel_fast_max_error", "sara_set_profiling", "sara_reset_profile",
-            "sara_read_profile", "sara_set_warm_start", "sara_warm_start_update",
+            "sara_read_profile", "sara_set_warm_start", "sara_warm_start_update", "sara_poll",
             "sara_destroy",
             "sara_last_error"]
 
@@ -78,7 +78,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "sara_read_rollouts": [P, P, P, P, P, P, P, P, P],
         "sara_read_logs": [P, P, I64, P, I64, P, I64, P, I64],
         "sara_read_advantages": [P, P, P, P, I32],
-        "sara_peff_batch": [P, P, I32, F64, F64, I32, P, P],
+        "sara_peff_batch": [P, P, P, P, I32, I32, P, P],
+        "sara_poll": [P, P],
         "grpo_group_advantages": [P, P, I32, F32, P, P],
         "sara_sample_logits": [P, I32, I32, P, P, U64, I32, F32, F32, I32, ctypes.c_uint32, P, P],
         "sara_gumbel_fast_max_error": [ctypes.POINTER(F64), P],
@@ -236,6 +237,14 @@ class Sara:
         _check(_lib.sara_query(self.h, ctypes.byref(st)), "sara_query")
         return {f: getattr(st, f) for f, _ in sara_step_stats._fields_ if f != "pad_"}
 
+    def sara_poll(self, h_pinned):
+        """Enqueue the asynchronous poll: h_pinned (a pinned host int32 tensor
+        of 2 elements) receives (done, device error word) when the stream
+        reaches it; returns at once."""
+        assert h_pinned.is_pinned() and h_pinned.numel() >= 2
+        self._in()
+        _check(_lib.sara_poll(self.h, _ptr(h_pinned)), "sara_poll")
+
     def sara_finish_step(self, eps=1e-6):
         self._in()
         _check(_lib.sara_finish_step(self.h, float(eps)), "sara_finish_step")
@@ -303,8 +312,9 @@ class Sara:
 
 
 # -- pure entry points ----------------------------------------------------------
-def sara_peff_batch(d_n, d_s, k, alpha0, beta0, d_out, stream=None):
-    _check(_lib.sara_peff_batch(_ptr(d_n), _ptr(d_s), int(k), float(alpha0), float(beta0), int(d_n.numel()),
+def sara_peff_batch(d_alpha, d_beta, d_n, d_s, k, d_out, stream=None):
+    """Eq. peff per prompt under its own prior Beta(d_alpha[i], d_beta[i])."""
+    _check(_lib.sara_peff_batch(_ptr(d_alpha), _ptr(d_beta), _ptr(d_n), _ptr(d_s), int(k), int(d_n.numel()),
                                 _ptr(d_out), _stream_handle(stream)), "sara_peff_batch")
 
 

@@ -393,10 +393,28 @@ __global__ __launch_bounds__(kCtlThreads) void k_refill(Ctl* __restrict__ ctl, c
 // ---------------------------------------------------------------------------
 // pure entry points
 // ---------------------------------------------------------------------------
-__global__ void k_peff(const int32_t* n, const int32_t* s, int k, double a0, double b0, int count,
-                       double* out) {
+// Eq. peff per prompt under that prompt's own prior; NaN for a prior that is
+// not positive and finite, or counts outside 0 <= s <= n <= k
+__global__ void k_peff(const double* alpha, const double* beta, const int32_t* n, const int32_t* s, int k,
+                       int count, double* out) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < count) out[i] = peff_dev(n[i], s[i], k, a0, b0);
+  if (i >= count) return;
+  const double a0 = alpha[i], b0 = beta[i];
+  const int ni = n[i], si = s[i];
+  const bool ok = a0 > 0.0 && b0 > 0.0 && isfinite(a0) && isfinite(b0) && si >= 0 && si <= ni && ni <= k;
+  out[i] = ok ? peff_dev(ni, si, k, a0, b0) : __builtin_nan("");
+}
+
+// error word, then (after a system-scope fence) the done flag, into pinned
+// host memory: a host that sees the flag change also sees the error word
+__global__ void k_poll(const Ctl* __restrict__ ctl, int32_t* h) {
+  if (threadIdx.x == 0) {
+    const int32_t err = __atomic_load_n(&ctl->error, __ATOMIC_RELAXED);
+    const int32_t done = __atomic_load_n(&ctl->done, __ATOMIC_RELAXED);
+    h[1] = err;
+    __threadfence_system();
+    h[0] = done;
+  }
 }
 
 // Eq. grpo: one wave per group, statistics in fp64
@@ -547,10 +565,15 @@ int launch_finish(sara_ctx* c, float eps) {
   return SARA_OK;
 }
 
-int launch_peff(const int32_t* n, const int32_t* s, int k, double a0, double b0, int count,
+int launch_peff(const double* alpha, const double* beta, const int32_t* n, const int32_t* s, int k, int count,
                 double* out, hipStream_t st) {
   if (count > 0)
-    hipLaunchKernelGGL(k_peff, dim3((count + 255) / 256), dim3(256), 0, st, n, s, k, a0, b0, count, out);
+    hipLaunchKernelGGL(k_peff, dim3((count + 255) / 256), dim3(256), 0, st, alpha, beta, n, s, k, count, out);
+  return SARA_OK;
+}
+
+int launch_poll(sara_ctx* c, int32_t* d_host) {
+  hipLaunchKernelGGL(k_poll, dim3(1), dim3(64), 0, c->stream, (const Ctl*)c->ctl, d_host);
   return SARA_OK;
 }
 

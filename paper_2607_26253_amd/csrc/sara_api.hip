@@ -700,14 +700,26 @@ extern "C" int sara_read_advantages(sara_ctx* c, int32_t* h_offsets, float* h_re
   return SARA_OK;
 }
 
-extern "C" int sara_peff_batch(const int32_t* d_n, const int32_t* d_s, int32_t k, double alpha0,
-                               double beta0, int32_t count, double* d_out, void* stream) {
+extern "C" int sara_peff_batch(const double* d_alpha, const double* d_beta, const int32_t* d_n,
+                               const int32_t* d_s, int32_t k, int32_t count, double* d_out, void* stream) {
   if (count < 0) return einval("count must be >= 0");
-  if (count > 0 && (!d_n || !d_s || !d_out)) return einval("null array");
+  if (count > 0 && (!d_alpha || !d_beta || !d_n || !d_s || !d_out)) return einval("null array");
   if (k < 1) return einval("k must be >= 1");
-  if (!(alpha0 > 0.0) || !(beta0 > 0.0)) return einval("alpha0 and beta0 must be > 0");
-  launch_peff(d_n, d_s, k, alpha0, beta0, count, d_out, (hipStream_t)stream);
+  launch_peff(d_alpha, d_beta, d_n, d_s, k, count, d_out, (hipStream_t)stream);
   HIP_TRY(hipGetLastError(), "peff launch");
+  return SARA_OK;
+}
+
+extern "C" int sara_poll(sara_ctx* c, int32_t* h_pinned) {
+  if (!c || !h_pinned) return einval("null argument");
+  if (!c->in_step) { set_error("sara_poll before sara_begin_step"); return SARA_ESTATE; }
+  void* d = nullptr;
+  if (hipHostGetDevicePointer(&d, h_pinned, 0) != hipSuccess || !d) {
+    (void)hipGetLastError();
+    return einval("h_pinned is not pinned host memory");
+  }
+  launch_poll(c, (int32_t*)d);
+  HIP_TRY(hipGetLastError(), "poll launch");
   return SARA_OK;
 }
 

@@ -222,8 +222,9 @@ int launch_warm_priors(sara_ctx* c);
 int launch_warm_update(sara_ctx* c, double lambda);
 int launch_refill(sara_ctx* c);
 int launch_finish(sara_ctx* c, float eps);
-int launch_peff(const int32_t* n, const int32_t* s, int k, double a0, double b0, int count,
+int launch_peff(const double* alpha, const double* beta, const int32_t* n, const int32_t* s, int k, int count,
                 double* out, hipStream_t st);
+int launch_poll(sara_ctx* c, int32_t* d_host);
 int launch_grpo(const float* r, const int32_t* off, int n_groups, float eps, float* adv,
                 hipStream_t st);
 int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* rid,

@@ -78,14 +78,16 @@ def test_wrong_weight_count_and_null_pointers():
 def test_pure_entry_points_validate_arguments():
     import paper_2607_26253_amd as sara
     L = sara._lib
-    assert L.sara_peff_batch(None, None, 8, 1.0, 1.0, -1, None, None) == sara.SARA_EINVAL
-    assert L.sara_peff_batch(None, None, 8, 1.0, 1.0, 4, None, None) == sara.SARA_EINVAL
-    assert L.sara_peff_batch(None, None, 8, 0.0, 1.0, 0, None, None) == sara.SARA_EINVAL
+    assert L.sara_peff_batch(None, None, None, None, 8, -1, None, None) == sara.SARA_EINVAL
+    assert L.sara_peff_batch(None, None, None, None, 8, 4, None, None) == sara.SARA_EINVAL
+    fake = ctypes.c_void_p(16)
+    assert L.sara_peff_batch(fake, None, fake, fake, 8, 4, fake, None) == sara.SARA_EINVAL
+    assert L.sara_peff_batch(fake, fake, fake, fake, 0, 4, fake, None) == sara.SARA_EINVAL
+    assert L.sara_poll(None, None) == sara.SARA_EINVAL
     assert L.grpo_group_advantages(None, None, -2, 1e-6, None, None) == sara.SARA_EINVAL
     assert L.grpo_group_advantages(None, None, 3, 1e-6, None, None) == sara.SARA_EINVAL
     assert L.sara_sample_logits(None, 4, 0, None, None, 0, 0, 1.0, 1.0, -1, 0, None, None) == sara.SARA_EINVAL
     # top_p outside (0, 1] is refused before anything is enqueued
-    fake = ctypes.c_void_p(16)
     for bad in (0.0, -0.5, 1.01):
         assert L.sara_sample_logits(fake, 4, 512, fake, fake, 0, 0, 1.0, bad, -1, 0, fake, None) == sara.SARA_EINVAL
     assert L.sara_set_warm_start(None, None, None, None, 0) == sara.SARA_EINVAL

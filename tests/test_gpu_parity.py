@@ -10,7 +10,7 @@ from oracle import grpo as OG
 from oracle import predictor as OP
 from oracle import run as ORUN
 from oracle import sampler as OS
-from tests.gpu_harness import compare_logs, device_setup, forced_table, run_gpu_step, slot_rows
+from tests.gpu_harness import compare_logs, device_setup, forced_table, run_gpu_step, slot_rows, upload_pool
 
 pytestmark = pytest.mark.gpu
 
@@ -24,21 +24,75 @@ def torch_cuda():
 
 
 def test_peff_batch_matches_oracle(torch_cuda):
+    """Eq. peff through the C ABI with a prior per prompt: shared priors over
+    every (n, s) of several k, then warm-start priors Beta(a0 + a, b0 + b)
+    with fractional pseudo-counts (the history warm start's carried counts),
+    each entry against the oracle within 1e-12; invalid entries give NaN."""
     import paper_2607_26253_amd as sara
     torch = torch_cuda
+
+    def run(al, be, ns, ss, k):
+        f64 = lambda v: torch.tensor(v, dtype=torch.float64, device="cuda")
+        i32 = lambda v: torch.tensor(v, dtype=torch.int32, device="cuda")
+        out = torch.empty(len(ns), dtype=torch.float64, device="cuda")
+        sara.sara_peff_batch(f64(al), f64(be), i32(ns), i32(ss), k, out)
+        return out.cpu().numpy()
+
     for (k, a0, b0) in [(8, 1.0, 1.0), (8, 0.3, 3.0), (16, 2.5, 0.7), (2, 1.0, 1.0), (31, 0.05, 7.5)]:
         ns, ss = [], []
         for n in range(0, k + 1):
             for s in range(0, n + 1):
                 ns.append(n)
                 ss.append(s)
-        d_n = torch.tensor(ns, dtype=torch.int32, device="cuda")
-        d_s = torch.tensor(ss, dtype=torch.int32, device="cuda")
-        out = torch.empty(len(ns), dtype=torch.float64, device="cuda")
-        sara.sara_peff_batch(d_n, d_s, k, a0, b0, out)
-        got = out.cpu().numpy()
+        got = run([a0] * len(ns), [b0] * len(ns), ns, ss, k)
         want = np.array([OP.p_eff(n, s, k, a0, b0) for n, s in zip(ns, ss)])
         assert np.max(np.abs(got - want)) <= 1e-12
+    g = np.random.default_rng(12)
+    m, k = 4000, 8
+    a = g.choice([0.0, 0.5, 1.75, 3.0, 6.25], m) * g.random(m)
+    b = g.choice([0.0, 0.5, 1.75, 3.0, 6.25], m) * g.random(m)
+    al, be = 1.0 + a, 1.0 + b
+    ns = g.integers(0, k + 1, m)
+    ss = np.array([g.integers(0, n + 1) for n in ns])
+    got = run(al.tolist(), be.tolist(), ns.tolist(), ss.tolist(), k)
+    want = np.array([OP.p_eff(int(n), int(s), k, x, y) for n, s, x, y in zip(ns, ss, al, be)])
+    assert np.max(np.abs(got - want)) <= 1e-12
+    bad = run([0.0, -1.0, float("inf"), 1.0, 1.0, 1.0], [1.0, 1.0, 1.0, float("nan"), 1.0, 1.0],
+              [0, 0, 0, 0, 3, 9], [0, 0, 0, 0, 4, 0], k)
+    assert np.all(np.isnan(bad))
+
+
+def test_poll_reports_done_flag_asynchronously(torch_cuda):
+    """sara_poll enqueues a write of (done, error word) into pinned host
+    memory and returns at once; the values agree with sara_query mid-step and
+    after the step has ended."""
+    import time
+    import paper_2607_26253_amd as sara
+    torch = torch_cuda
+    cfg, w, pool, seed = _tiny()
+    ctx, _ = device_setup(cfg, w)
+    d_tok, d_p, d_fl = upload_pool(pool)
+    h = torch.full((2,), -7, dtype=torch.int32).pin_memory()
+    ctx.sara_begin_step(d_tok, pool["offsets"], d_p, d_fl, pool["step"])
+
+    def poll():
+        h[0] = -1
+        ctx.sara_poll(h)
+        t0 = time.time()
+        while int(h[0]) == -1:
+            assert time.time() - t0 < 30.0, "poll flag never arrived"
+        return int(h[0]), int(h[1])
+
+    for _ in range(5):
+        ctx.sara_decode_step(None, None, False)
+        ctx.sara_posterior_decide()
+        ctx.sara_refill()
+    assert poll() == (0, 0)
+    assert ctx.sara_query()["done"] == 0
+    ctx.sara_run(None, graph_iters=8)
+    assert poll() == (1, 0)
+    assert ctx.sara_query()["done"] == 1
+    ctx.close()
 
 
 def test_grpo_matches_oracle(torch_cuda):

@@ -106,13 +106,31 @@ def test_conjugacy():
         a, b = P.posterior(n, s, a0, b0)
         for x in (0.05, 0.3, 0.5, 0.77, 0.95):
             assert float(prior(x) * lik(x) / Z) == pytest.approx(stats.beta.pdf(x, a, b), rel=1e-9)
-    # sequential updates commute: any order of the same outcomes gives one posterior
-    outs = [1, 0, 0, 1, 1, 0, 1]
-    for perm in itertools.permutations(outs, len(outs)):
-        n = len(perm)
-        s = sum(perm)
-        assert P.posterior(n, s) == (1 + 4, 1 + 3)
-        break
+    # sequential updates commute: folding the outcomes in one at a time by
+    # Bayes' rule on a grid (prior density times the likelihood of a single
+    # outcome), in several orders, leaves a density proportional to the
+    # Beta(a0 + s, b0 + n - s) density; the closed-form update applied one
+    # observation at a time lands on the same parameters
+    x = (np.arange(20000) + 0.5) / 20000
+    rng = random.Random(11)
+    for (a0, b0) in [(1.0, 1.0), (0.3, 3.0), (2.5, 0.7)]:
+        outs = [1, 0, 0, 1, 1, 0, 1]
+        want = stats.beta.pdf(x, *P.posterior(len(outs), sum(outs), a0, b0))
+        perms = set()
+        while len(perms) < 6:
+            perm = outs[:]
+            rng.shuffle(perm)
+            perms.add(tuple(perm))
+        for perm in perms:
+            f = stats.beta.pdf(x, a0, b0)
+            a, b = a0, b0
+            for o in perm:
+                f = f * (x if o else 1.0 - x)
+                f = f / f.sum()
+                a, b = P.posterior(1, o, a, b)
+            assert (a, b) == P.posterior(len(outs), sum(outs), a0, b0)
+            ratio = f[100:-100] / want[100:-100]
+            assert ratio.max() / ratio.min() - 1.0 < 1e-9
 
 
 def test_monotone_and_absorbing():
@@ -189,4 +207,11 @@ def test_priority_key():
     assert P.priority_key(1.0) == 1 << 20
     assert P.priority_key(0.0) == 0
     assert P.priority_key(0.5) == 1 << 19
-    assert P.priority_key(7 / 9) == round(7 / 9 * (1 << 20))
+    # round half up, not floor: 2^20 * 2/3 = 699050.67, 2^20 * 4/9 = 466033.78,
+    # 2^20 * 5/9 = 582542.22, and 1.5 / 2^20 sits on a half
+    assert P.priority_key(2 / 3) == 699051
+    assert P.priority_key(4 / 9) == 466034
+    assert P.priority_key(5 / 9) == 582542
+    assert P.priority_key(7 / 9) == 815559
+    assert P.priority_key(1.5 / (1 << 20)) == 2
+    assert P.priority_key(2 / 3, bits=4) == 11
