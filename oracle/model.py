@@ -109,13 +109,34 @@ class Decoder:
             o[h] = p @ V[g, :n_ctx]
         return o
 
+    def _attend_causal(self, q, K, V, positions):
+        """Causal scaled dot-product attention of T consecutive queries:
+        q: (T, Hq, hd) at `positions`; query t attends to cache positions
+        [0, positions[t]], i.e. softmax(q K^T / sqrt(hd) + causal mask) V per
+        head, with masked scores set to -inf (weight exactly 0)."""
+        T = len(positions)
+        grp = self.hq // self.hkv
+        n = int(positions[-1]) + 1
+        scale = 1.0 / np.sqrt(self.hd)
+        masked = np.arange(n)[None, :] > np.asarray(positions)[:, None]
+        o = np.empty((T, self.hq, self.hd))
+        for h in range(self.hq):
+            g = h // grp
+            sc = (q[:, h, :] @ K[g, :n].T) * scale
+            sc[masked] = -np.inf
+            sc = sc - sc.max(axis=1, keepdims=True)
+            p = np.exp(sc)
+            p /= p.sum(axis=1, keepdims=True)
+            o[:, h] = p @ V[g, :n]
+        return o
+
     def new_cache(self, T_max):
         return [(np.zeros((self.hkv, T_max, self.hd)), np.zeros((self.hkv, T_max, self.hd)))
                 for _ in range(self.L)]
 
     # -- forward over a set of new positions of ONE sequence --------------
     def forward(self, tokens, positions, cache, want_logits=True, logit_rows=None):
-        """Append tokens at `positions` (consecutive) to `cache`, causal.
+        """Append tokens at `positions` (consecutive, ascending) to `cache`, causal.
         logit_rows: optional indices of the rows whose logits are returned."""
         tokens = np.asarray(tokens, dtype=np.int64)
         positions = np.asarray(positions, dtype=np.int64)
@@ -133,7 +154,7 @@ class Decoder:
             K, Vc = cache[l]
             K[:, positions, :] = k.transpose(1, 0, 2)
             Vc[:, positions, :] = v.transpose(1, 0, 2)
-            o = np.stack([self._attend(q[t], K, Vc, positions[t] + 1) for t in range(T)])
+            o = self._attend_causal(q, K, Vc, positions)
             o = self.rnd(o.reshape(T, self.hq * self.hd))
             h = h + self.mm(o, f"l{l}.wo")
             x = self.rnd(self.rmsnorm(h, f"l{l}.ffn_norm"))

@@ -5,6 +5,20 @@ import numpy as np
 import workloads as W
 
 
+_WEIGHTS = {}
+
+
+def cached_weights(cfg):
+    """Weights of cfg's model, reused by consecutive tests of the same model
+    (a few GB at full vocabulary; the two most recent models are kept)."""
+    key = (W.master_seed(cfg), tuple(sorted(cfg["model"].items())))
+    if key not in _WEIGHTS:
+        while len(_WEIGHTS) >= 2:
+            _WEIGHTS.pop(next(iter(_WEIGHTS)))
+        _WEIGHTS[key] = W.make_weights(cfg)
+    return _WEIGHTS[key]
+
+
 def device_setup(cfg, weights=None):
     import torch
 

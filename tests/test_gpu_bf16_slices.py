@@ -2,16 +2,20 @@
 vocabulary) with reduced allocation sizes the CPU oracle can generate token
 by token.  Teacher forcing from the oracle's tokens.
 
-Logit tolerance.  The stated bound is 3e-2 * rms(logits).  A random-init
-28/36-layer bf16 decoder amplifies last-bit rounding differences: the oracle
-itself moves by up to ~5% of rms in max-norm when only its GEMM accumulation
-changes from fp32 to fp64.  So at full depth the bound is read as a per-row
-relative RMS error (||d||_2 / ||oracle||_2 <= 3e-2), with the max-norm held
-to twice the oracle's own fp32-vs-fp64 spread on the same rows; a 2-layer
-truncation at full width and vocabulary, where rounding noise does not
-compound, must meet max|d| <= 3e-2 * rms strictly.  Decisions, rewards and
-lengths are bit-exact; the sampler fed the oracle's logits reproduces the
-oracle's tokens (near ties excepted)."""
+Logit tolerance.  The stated bound is max|d| <= 3e-2 * rms(logits) per row.
+The 2-layer tests at full width and vocabulary meet it: the truncations,
+top-p, long-context and full-length-context cases.  At full depth (28 and
+36 layers) it cannot be met by any implementation that rounds differently
+from the oracle in the last bit.  A random-init bf16 decoder of that depth
+amplifies rounding: the oracle moves by 5.7-9.9% of rms in max-norm when only
+its GEMM accumulation changes from fp32 to fp64.  At full depth each slice
+therefore has two fixed bounds:
+* relative RMS error ||d||_2 / ||oracle||_2 <= 3e-2;
+* max|d| <= FULL_DEPTH_MAX_REL[slice] * rms.
+The latter is 1.5x the oracle's own fp32-vs-fp64 spread measured on the same
+rows, rounded up to 0.01.  That spread is printed beside the GPU's error on
+every run.  Decisions, rewards and lengths are bit-exact.  The sampler fed
+the oracle's logits reproduces the oracle's tokens (near ties excepted)."""
 import copy
 
 import numpy as np
@@ -20,7 +24,7 @@ import pytest
 import workloads as W
 from oracle import run as ORUN
 from oracle import sampler as OS
-from tests.gpu_harness import compare_logs, device_setup, forced_table, run_gpu_step, slot_rows
+from tests.gpu_harness import cached_weights, compare_logs, device_setup, forced_table, run_gpu_step, slot_rows
 
 pytestmark = pytest.mark.gpu
 
@@ -29,6 +33,16 @@ SLICES = {
     "qwen3b_shape": dict(B=2, N=16, max_new=8),
     "long_ragged_1p5b": dict(B=3, N=24, max_new=10, slots=6),
     "pool_3b": dict(B=2, N=16, max_new=8, prompt_len=(24, 48)),
+}
+
+
+# max|d| / rms bounds at full depth (1.5 x the oracle's fp32-vs-fp64 spread:
+# 0.0722, 0.0939, 0.0565, 0.0990 measured on these slices' rows)
+FULL_DEPTH_MAX_REL = {
+    "qwen1p5b_shape": 0.11,
+    "qwen3b_shape": 0.15,
+    "long_ragged_1p5b": 0.09,
+    "pool_3b": 0.15,
 }
 
 
@@ -133,7 +147,7 @@ def test_bf16_slice_full_depth(name):
     print(f"[slice] rel-rms err max {worst_rms:.4f}; max|d|/rms {worst_max:.4f}; "
           f"oracle fp32-vs-fp64 floor {floor:.4f}", flush=True)
     assert worst_rms <= 3e-2
-    assert worst_max <= max(3e-2, 2.0 * floor)
+    assert worst_max <= FULL_DEPTH_MAX_REL[name]
     check_sampler_on_oracle_logits(cfg, ora, seed, pool["step"])
     n = check_fused_sampler_exact(cfg, gpu, seed, pool["step"])
     print(f"[slice] fused LM-head sampler = exact sampler on {n} GPU logit rows", flush=True)
@@ -151,7 +165,7 @@ def test_bf16_slice_full_depth(name):
 @pytest.mark.parametrize("name", ["qwen1p5b_shape", "qwen3b_shape"])
 def test_bf16_two_layer_truncation_strict(name):
     cfg = slice_cfg(name, layers=2)
-    w = W.make_weights(cfg)
+    w = cached_weights(cfg)
     pool = W.make_pool(cfg, 0)
     seed = W.sampling_seed(cfg)
     ora = ORUN.run_step(cfg, w, pool, seed, keep_logits=lambda u, j, i: True)
@@ -176,7 +190,7 @@ def test_bf16_two_layer_top_p():
     without a caller logits buffer (library buffer) gives the same rollouts."""
     cfg = slice_cfg("qwen1p5b_shape", layers=2)
     cfg["alloc"]["top_p"] = 0.9
-    w = W.make_weights(cfg)
+    w = cached_weights(cfg)
     pool = W.make_pool(cfg, 0)
     seed = W.sampling_seed(cfg)
     ora = ORUN.run_step(cfg, w, pool, seed, keep_logits=lambda u, j, i: True)
@@ -213,7 +227,7 @@ def test_bf16_two_layer_long_context_strict():
     full = W.get_config("qwen1p5b_shape")
     cfg = W.parity_slice(full, B=2, N=16, prompt_len=(300, 720), max_new=40, pool_U=8)
     cfg["model"]["n_layers"] = 2
-    w = W.make_weights(cfg)
+    w = cached_weights(cfg)
     pool = W.make_pool(cfg, 0)
     plen = np.diff(pool["offsets"])
     assert plen.min() - 1 > 8 * 16      # more than one split of 8 pages for every row
@@ -227,6 +241,54 @@ def test_bf16_two_layer_long_context_strict():
     worst_max = max(e["max"] for e in errs)
     print(f"[slice-2L-long] {len(errs)} rows, prompts {plen.min()}-{plen.max()}: max|d|/rms {worst_max:.4f}",
           flush=True)
+    assert worst_max <= 3e-2
+    check_fused_sampler_exact(cfg, gpu, seed, pool["step"])
+    ctx.close()
+
+
+# prompt lengths of the full-length case: the longest context reaches the
+# long-rollout workload's range (prompt 4590 + 20 new tokens, 37 pages of
+# 128-token splits), every decode row has more than 8 splits (the merge runs
+# several batches of 8), and the pool's 7,387 prompt rows cross the 4,096-row
+# prefill chunk inside prompt 1
+FULL_LENGTH_PROMPTS = [1100, 4590, 1700]
+PREFILL_CHUNK_ROWS = 4096
+SPLIT_TOKENS = 8 * 16
+
+
+@pytest.mark.parametrize("name", ["qwen1p5b_shape", "qwen3b_shape"])
+def test_bf16_two_layer_full_length_contexts(name):
+    """2 layers at the model's full width and vocabulary, teacher forced from
+    the oracle, with contexts of 1,100-4,610 tokens: decode attention over up
+    to 37 context splits (the split merge's later batches of 8), a prompt
+    prefilled across two 4,096-row chunks, every row's logits within
+    3e-2 * rms element-wise, logs bit-exact, fused sampler = exact sampler."""
+    lens = FULL_LENGTH_PROMPTS
+    full = W.get_config(name)
+    cfg = W.parity_slice(full, B=len(lens), N=8 * len(lens), prompt_len=(min(lens), max(lens)), max_new=20,
+                         pool_U=len(lens))
+    cfg["model"]["n_layers"] = 2
+    pool = W.pool_with_lengths(cfg, lens, 0)
+    rows = np.concatenate([[0], np.cumsum(np.array(lens) - 1)])
+    straddle = [u for u in range(len(lens))
+                if rows[u] // PREFILL_CHUNK_ROWS != (rows[u + 1] - 1) // PREFILL_CHUNK_ROWS]
+    assert straddle, "no prompt crosses a prefill chunk"
+    assert min(lens) - 1 > 8 * SPLIT_TOKENS       # every row: more than one batch of 8 splits
+    w = cached_weights(cfg)
+    seed = W.sampling_seed(cfg)
+    print(f"[full-length] {name}: prompts {lens}, prompts crossing a prefill chunk {straddle}", flush=True)
+    ora = ORUN.run_step(cfg, w, pool, seed, keep_logits=lambda u, j, i: True)
+    ctx, _ = device_setup(cfg, w)
+    gpu = run_gpu_step(ctx, cfg, pool, forced=forced_table(cfg, ora["rollouts_detail"]), capture_logits=True)
+    compare_logs(gpu["logs"], ora)
+    errs = row_errors(gpu, ora["logits"])
+    worst_max = max(e["max"] for e in errs)
+    ctxs = [lens[u] - 1 + i for (u, j, i) in slot_rows(gpu).values()]
+    drawn = sorted({u for (u, j, i) in slot_rows(gpu).values()})
+    print(f"[full-length] {name}: {len(errs)} rows, prompts drawn {drawn}, contexts {min(ctxs)}-{max(ctxs)} "
+          f"({-(-min(ctxs) // SPLIT_TOKENS)}-{-(-max(ctxs) // SPLIT_TOKENS)} splits): max|d|/rms {worst_max:.4f}",
+          flush=True)
+    assert 1 in drawn and max(ctxs) >= 4589
     assert worst_max <= 3e-2
     check_fused_sampler_exact(cfg, gpu, seed, pool["step"])
     ctx.close()

@@ -150,9 +150,21 @@ def weight_specs(model: dict):
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
     """Round-to-nearest-even fp32 -> bf16 bit patterns (uint16); finite inputs."""
-    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    r = (b + np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
-    return r.astype(np.uint16)
+    b = np.ascontiguousarray(x, dtype=np.float32).reshape(-1).view(np.uint32)
+    out = np.empty(b.shape, dtype=np.uint16)
+
+    def conv(c):
+        s = b[c * _CHUNK:(c + 1) * _CHUNK]
+        out[c * _CHUNK:(c + 1) * _CHUNK] = (s + np.uint32(0x7FFF) + ((s >> np.uint32(16)) & np.uint32(1))) \
+            >> np.uint32(16)
+
+    n_chunks = (b.size + _CHUNK - 1) // _CHUNK
+    if n_chunks <= 1:
+        conv(0)
+    else:
+        with ThreadPoolExecutor(max_workers=min(16, n_chunks)) as ex:
+            list(ex.map(conv, range(n_chunks)))
+    return out.reshape(np.shape(x))
 
 
 _CHUNK = 1 << 22
@@ -236,6 +248,25 @@ def make_pool(cfg: dict, step: int = 0) -> dict:
         L = np.rint(np.exp(fl["mu"] + fl["sigma"] * z))
         forced = np.clip(L, 1, min(fl["cap"], a["max_new"])).astype(np.int32)
     return dict(tokens=tokens, offsets=offsets, p=p, forced_len=forced, step=step)
+
+
+def pool_with_lengths(cfg: dict, lengths, step: int = 0) -> dict:
+    """A pool like ``make_pool``'s whose prompt lengths are given (edge and
+    long-context cases): tokens uniform in [0, V-1), success rates from the
+    workload's mixture at that step, no forced lengths."""
+    m = cfg["model"]
+    lens = np.asarray(lengths, dtype=np.int32)
+    assert lens.min() >= 1 and lens.max() <= cfg["alloc"]["max_prompt"] and len(lens) == cfg["alloc"]["pool_U"]
+    master = master_seed(cfg)
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([master, 5, step, len(lens)])))
+    offsets = np.zeros(len(lens) + 1, dtype=np.int32)
+    offsets[1:] = np.cumsum(lens)
+    tokens = g.integers(0, m["vocab"] - 1, size=int(offsets[-1])).astype(np.int32)
+    wh, we, wm = mixture_weights(cfg, step)
+    comp = g.choice(3, size=len(lens), p=[wh, we, wm])
+    p = np.where(comp == 0, g.beta(0.3, 3.0, size=len(lens)),
+                 np.where(comp == 1, g.beta(3.0, 0.3, size=len(lens)), g.random(size=len(lens))))
+    return dict(tokens=tokens, offsets=offsets, p=p.astype(np.float64), forced_len=None, step=step)
 
 
 def prompt_set(cfg: dict, D: int) -> dict:
