@@ -314,6 +314,29 @@ int sara_sample_logits(const float* d_logits, int32_t n_rows, int32_t vocab,
                        int32_t step_index, float temperature, float top_p, int32_t eos_id,
                        uint32_t forced_eos_u32, int32_t* d_tok, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * sampler of sara_sample_logits with the same arguments and results, whose
+ * buffers (row count, per-row chunk winners, top-p histograms and state)
+ * live in one static device array per GPU of SARA_NOALLOC_SCRATCH_BYTES
+ * bytes, held from the first call on a device until the process ends.  It
+ * calls no allocating routine and does not synchronise: the work is
+ * enqueued on stream (which must belong to the current device) and d_tok is
+ * valid once the stream has passed it.
+ * Limits: n_rows <= SARA_NOALLOC_MAX_ROWS, and n_rows <=
+ * SARA_NOALLOC_MAX_TOPP_ROWS when top_p < 1; larger inputs, like the
+ * argument errors of sara_sample_logits, return SARA_EINVAL and enqueue
+ * nothing.  Every call on one GPU shares that GPU's array: calls whose work
+ * overlaps on the device (other streams, other threads) race and give
+ * undefined tokens; calls ordered on one stream are safe. */
+#define SARA_NOALLOC_MAX_ROWS 4096
+#define SARA_NOALLOC_MAX_TOPP_ROWS 64
+#define SARA_NOALLOC_SCRATCH_BYTES 17307136
+int sara_sample_logits_noalloc(const float* d_logits, int32_t n_rows, int32_t vocab,
+                               const int32_t* d_rid, const int32_t* d_pos, uint64_t seed,
+                               int32_t step_index, float temperature, float top_p, int32_t eos_id,
+                               uint32_t forced_eos_u32, int32_t* d_tok, void* stream);
+
 /* Self-check of the fused LM-head sampler (bf16 models).  That sampler
  * scores every vocabulary id with an fp32 estimate of the Gumbel noise and
  * re-scores exactly (fp64 noise rounded to fp32, the definition of the noise

@@ -24,7 +24,7 @@ SARA_COMMIT, SARA_ABANDON, SARA_CONTINUE = 1, 2, 3
 EXPORTED = ["sara_init", "sara_begin_step", "sara_decode_step", "sara_posterior_decide",
             "sara_refill", "sara_run", "sara_query", "sara_finish_step", "sara_read_rollouts",
             "sara_read_logs", "sara_read_advantages", "sara_peff_batch", "grpo_group_advantages",
-            "sara_sample_logits", "sara_gumbel_fast_max_error", "sara_set_profiling", "sara_reset_profile",
+            "sara_sample_logits", "sara_sample_logits_noalloc", "sara_gumbel_fast_max_error", "sara_set_profiling", "sara_reset_profile",
             "sara_read_profile", "sara_set_warm_start", "sara_warm_start_update", "sara_poll",
             "sara_destroy",
             "sara_last_error"]
@@ -82,6 +82,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "sara_poll": [P, P],
         "grpo_group_advantages": [P, P, I32, F32, P, P],
         "sara_sample_logits": [P, I32, I32, P, P, U64, I32, F32, F32, I32, ctypes.c_uint32, P, P],
+        "sara_sample_logits_noalloc": [P, I32, I32, P, P, U64, I32, F32, F32, I32, ctypes.c_uint32, P, P],
         "sara_gumbel_fast_max_error": [ctypes.POINTER(F64), P],
         "sara_set_profiling": [P, I32],
         "sara_reset_profile": [P],
@@ -337,3 +338,19 @@ def sara_sample_logits(d_logits, d_rid, d_pos, seed, step_index, temperature, eo
                                    int(seed) & ((1 << 64) - 1), int(step_index), float(temperature),
                                    float(top_p), int(eos_id), int(forced_eos_u32), _ptr(d_tok), _stream_handle(stream)),
            "sara_sample_logits")
+
+
+# limits of the allocation-free sampler (include/sara.h)
+NOALLOC_MAX_ROWS, NOALLOC_MAX_TOPP_ROWS = 4096, 64
+
+
+def sara_sample_logits_noalloc(d_logits, d_rid, d_pos, seed, step_index, temperature, eos_id, forced_eos_u32,
+                               d_tok, stream=None, top_p=1.0):
+    """The stand-alone sampler over the library's static scratch (no
+    allocation, no synchronisation): enqueued on stream."""
+    n, V = d_logits.shape
+    _check(_lib.sara_sample_logits_noalloc(_ptr(d_logits), int(n), int(V), _ptr(d_rid), _ptr(d_pos),
+                                           int(seed) & ((1 << 64) - 1), int(step_index), float(temperature),
+                                           float(top_p), int(eos_id), int(forced_eos_u32), _ptr(d_tok),
+                                           _stream_handle(stream)),
+           "sara_sample_logits_noalloc")

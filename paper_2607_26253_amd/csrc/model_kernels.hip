@@ -13,6 +13,8 @@
 // bf16 MFMA (v_mfma_f32_16x16x32_bf16) with fp32 accumulation; split-K
 // partials go to a workspace and are summed in split order by the epilogue,
 // so results do not depend on scheduling.  The fp32 model uses a VALU GEMM.
+#include <mutex>
+
 #include "sara_internal.h"
 
 #include <hip/hip_ext.h>
@@ -2341,62 +2343,148 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
   return SARA_OK;
 }
 
+// Buffers of the stand-alone sampler: the live row count, per-row chunk
+// winners and, for top-p < 1, the descent's chunk maxima, histograms and
+// per-row state.  Every kernel below writes a buffer before reading it, so
+// the contents left by an earlier call never matter.
+struct SampleBufs {
+  int32_t* mdev;
+  float* best;
+  int32_t* bidx;
+  float* pmax;
+  unsigned long long* hist;
+  unsigned long long* state;   // per row: above, target
+  uint32_t* thr;
+};
+
+__global__ void k_set_count(int32_t* __restrict__ dst, int n) {
+  if (threadIdx.x == 0) dst[0] = n;
+}
+
+static void enqueue_sample_rows(const SampleBufs& b, const float* logits, int n_rows, int V, const int32_t* rid,
+                                const int32_t* pos, uint64_t seed, int step, float temp, float top_p, int eos,
+                                uint32_t feos, int32_t* tok, hipStream_t st) {
+  hipLaunchKernelGGL(k_set_count, dim3(1), dim3(64), 0, st, b.mdev, n_rows);
+  const bool topp = top_p < 1.0f;
+  if (topp) {
+    const int g = std::min(n_rows * kTopPChunks, 2048);
+    hipLaunchKernelGGL(k_topp_max, dim3(g), dim3(256), 0, st, (const int32_t*)b.mdev, (const RowDesc*)nullptr,
+                       logits, V, 0, (const CtlParams*)nullptr, temp, b.pmax);
+    for (int d = 0; d < 3; ++d) {
+      hipLaunchKernelGGL(k_topp_hist, dim3(g), dim3(256), 0, st, (const int32_t*)b.mdev, (const RowDesc*)nullptr,
+                         logits, V, 0, (const CtlParams*)nullptr, temp, (const float*)b.pmax, d,
+                         (const uint32_t*)b.thr, b.hist);
+      hipLaunchKernelGGL(k_topp_pick, dim3(std::min(n_rows, 1024)), dim3(kTopPThreads), 0, st,
+                         (const int32_t*)b.mdev, (const CtlParams*)nullptr, top_p, d,
+                         (const unsigned long long*)b.hist, b.thr, b.state, b.state + n_rows);
+    }
+  }
+  hipLaunchKernelGGL(k_sample_partial, dim3(std::min(n_rows * kSampleChunks, 2048)), dim3(256), 0, st,
+                     (const int32_t*)b.mdev, rid, pos, (const RowDesc*)nullptr, logits, V, 0,
+                     topp ? (const uint32_t*)b.thr : (const uint32_t*)nullptr, (const CtlParams*)nullptr, seed,
+                     step, temp, b.best, b.bidx);
+  hipLaunchKernelGGL(k_sample_rows_final, dim3((n_rows + 255) / 256), dim3(256), 0, st, n_rows, rid,
+                     pos, b.best, b.bidx, kSampleChunks, seed, step, eos, feos, tok);
+}
+
 int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* rid,
                        const int32_t* pos, uint64_t seed, int step, float temp, float top_p, int eos,
                        uint32_t feos, int32_t* tok, hipStream_t st) {
-  float* best = nullptr;
-  int32_t* bidx = nullptr;
-  int32_t* mdev = nullptr;
-  hipError_t e = hipMallocAsync((void**)&best, sizeof(float) * (size_t)n_rows * kSampleChunks, st);
-  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
-  e = hipMallocAsync((void**)&bidx, sizeof(int32_t) * (size_t)n_rows * kSampleChunks, st);
-  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
-  e = hipMallocAsync((void**)&mdev, sizeof(int32_t), st);
-  if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
-  e = hipMemcpyAsync(mdev, &n_rows, sizeof(int32_t), hipMemcpyHostToDevice, st);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  SampleBufs b{};
+  std::vector<void*> owned;
+  auto get = [&](void** p, size_t bytes) -> hipError_t {
+    hipError_t e = hipMallocAsync(p, bytes, st);
+    if (e == hipSuccess) owned.push_back(*p);
+    return e;
+  };
+  auto release = [&]() {
+    for (void* q : owned) (void)hipFreeAsync(q, st);
+  };
   const bool topp = top_p < 1.0f;
-  float* pmax = nullptr;
-  unsigned long long* hist = nullptr;
-  unsigned long long* state = nullptr;   // per row: above, target
-  uint32_t* thr = nullptr;
-  if (topp) {
-    e = hipMallocAsync((void**)&pmax, sizeof(float) * (size_t)n_rows * kTopPChunks, st);
-    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
-    e = hipMallocAsync((void**)&hist, sizeof(unsigned long long) * (size_t)n_rows * kTopPChunks * kTopPBins, st);
-    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
-    e = hipMallocAsync((void**)&state, sizeof(unsigned long long) * 2 * (size_t)n_rows, st);
-    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
-    e = hipMallocAsync((void**)&thr, sizeof(uint32_t) * (size_t)n_rows, st);
-    if (e != hipSuccess) return hip_fail(e, "hipMallocAsync");
-    const int g = std::min(n_rows * kTopPChunks, 2048);
-    hipLaunchKernelGGL(k_topp_max, dim3(g), dim3(256), 0, st, (const int32_t*)mdev, (const RowDesc*)nullptr,
-                       logits, V, 0, (const CtlParams*)nullptr, temp, pmax);
-    for (int d = 0; d < 3; ++d) {
-      hipLaunchKernelGGL(k_topp_hist, dim3(g), dim3(256), 0, st, (const int32_t*)mdev, (const RowDesc*)nullptr,
-                         logits, V, 0, (const CtlParams*)nullptr, temp, (const float*)pmax, d,
-                         (const uint32_t*)thr, hist);
-      hipLaunchKernelGGL(k_topp_pick, dim3(std::min(n_rows, 1024)), dim3(kTopPThreads), 0, st,
-                         (const int32_t*)mdev, (const CtlParams*)nullptr, top_p, d,
-                         (const unsigned long long*)hist, thr, state, state + n_rows);
-    }
+  hipError_t e = get((void**)&b.mdev, sizeof(int32_t));
+  if (e == hipSuccess) e = get((void**)&b.best, sizeof(float) * (size_t)n_rows * kSampleChunks);
+  if (e == hipSuccess) e = get((void**)&b.bidx, sizeof(int32_t) * (size_t)n_rows * kSampleChunks);
+  if (e == hipSuccess && topp) e = get((void**)&b.pmax, sizeof(float) * (size_t)n_rows * kTopPChunks);
+  if (e == hipSuccess && topp)
+    e = get((void**)&b.hist, sizeof(unsigned long long) * (size_t)n_rows * kTopPChunks * kTopPBins);
+  if (e == hipSuccess && topp) e = get((void**)&b.state, sizeof(unsigned long long) * 2 * (size_t)n_rows);
+  if (e == hipSuccess && topp) e = get((void**)&b.thr, sizeof(uint32_t) * (size_t)n_rows);
+  if (e != hipSuccess) {
+    release();
+    return hip_fail(e, "hipMallocAsync");
   }
-  hipLaunchKernelGGL(k_sample_partial, dim3(std::min(n_rows * kSampleChunks, 2048)), dim3(256), 0, st, mdev,
-                     rid, pos, (const RowDesc*)nullptr, logits, V, 0, (const uint32_t*)thr,
-                     (const CtlParams*)nullptr, seed, step, temp, best, bidx);
-  hipLaunchKernelGGL(k_sample_rows_final, dim3((n_rows + 255) / 256), dim3(256), 0, st, n_rows, rid,
-                     pos, best, bidx, kSampleChunks, seed, step, eos, feos, tok);
-  if (topp) {
-    (void)hipFreeAsync(pmax, st);
-    (void)hipFreeAsync(hist, st);
-    (void)hipFreeAsync(state, st);
-    (void)hipFreeAsync(thr, st);
-  }
-  (void)hipFreeAsync(best, st);
-  (void)hipFreeAsync(bidx, st);
-  (void)hipFreeAsync(mdev, st);
+  enqueue_sample_rows(b, logits, n_rows, V, rid, pos, seed, step, temp, top_p, eos, feos, tok, st);
+  e = hipGetLastError();
+  release();
+  if (e != hipSuccess) return hip_fail(e, "sample_rows launch");
   e = hipStreamSynchronize(st);
   if (e != hipSuccess) return hip_fail(e, "sample_rows");
+  return SARA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// The stand-alone sampler without allocation: its buffers live in one static
+// device array per GPU (this file's `scratch`, sized for kNoAllocMaxRows rows
+// at top_p = 1 and kNoAllocMaxToppRows rows with the top-p passes).  Host code
+// never passes the array's name to a kernel: the address each device gives
+// for it is looked up once per device and kept.
+// ---------------------------------------------------------------------------
+namespace {
+constexpr size_t kAlign = 256;
+constexpr size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+constexpr size_t kOffCount = 0;
+constexpr size_t kOffBest = kAlign;
+constexpr size_t kOffBidx = kOffBest + align_up(sizeof(float) * (size_t)kNoAllocMaxRows * kSampleChunks);
+constexpr size_t kOffPmax = kOffBidx + align_up(sizeof(int32_t) * (size_t)kNoAllocMaxRows * kSampleChunks);
+constexpr size_t kOffHist = kOffPmax + align_up(sizeof(float) * (size_t)kNoAllocMaxToppRows * kTopPChunks);
+constexpr size_t kOffState =
+    kOffHist + align_up(sizeof(unsigned long long) * (size_t)kNoAllocMaxToppRows * kTopPChunks * kTopPBins);
+constexpr size_t kOffThr = kOffState + align_up(sizeof(unsigned long long) * 2 * (size_t)kNoAllocMaxToppRows);
+constexpr size_t kScratchBytes = kOffThr + align_up(sizeof(uint32_t) * (size_t)kNoAllocMaxToppRows);
+static_assert(kScratchBytes == kNoAllocScratchBytes, "scratch layout and its stated size disagree");
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxScratchDevices] = {};
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// Device address of `scratch` on the current device, looked up on the first
+// call on that device.
+static int scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxScratchDevices) return hip_fail(hipErrorInvalidDevice, "device index");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return hip_fail(e != hipSuccess ? e : hipErrorInvalidSymbol, "hipGetSymbolAddress");
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return SARA_OK;
+}
+
+int launch_sample_rows_noalloc(const float* logits, int n_rows, int V, const int32_t* rid, const int32_t* pos,
+                               uint64_t seed, int step, float temp, float top_p, int eos, uint32_t feos,
+                               int32_t* tok, hipStream_t st) {
+  void* base = nullptr;
+  int rc = scratch_address(&base);
+  if (rc != SARA_OK) return rc;
+  unsigned char* b8 = (unsigned char*)base;
+  SampleBufs b{};
+  b.mdev = (int32_t*)(b8 + kOffCount);
+  b.best = (float*)(b8 + kOffBest);
+  b.bidx = (int32_t*)(b8 + kOffBidx);
+  b.pmax = (float*)(b8 + kOffPmax);
+  b.hist = (unsigned long long*)(b8 + kOffHist);
+  b.state = (unsigned long long*)(b8 + kOffState);
+  b.thr = (uint32_t*)(b8 + kOffThr);
+  enqueue_sample_rows(b, logits, n_rows, V, rid, pos, seed, step, temp, top_p, eos, feos, tok, st);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "sample_rows_noalloc launch");
   return SARA_OK;
 }
 

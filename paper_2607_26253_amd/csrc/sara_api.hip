@@ -747,6 +747,32 @@ extern "C" int sara_sample_logits(const float* d_logits, int32_t n_rows, int32_t
                             forced_eos_u32, d_tok, (hipStream_t)stream);
 }
 
+extern "C" int sara_sample_logits_noalloc(const float* d_logits, int32_t n_rows, int32_t vocab,
+                                          const int32_t* d_rid, const int32_t* d_pos, uint64_t seed,
+                                          int32_t step_index, float temperature, float top_p, int32_t eos_id,
+                                          uint32_t forced_eos_u32, int32_t* d_tok, void* stream) {
+  if (n_rows < 0 || vocab < 1) return einval("n_rows must be >= 0 and vocab >= 1");
+  if (n_rows == 0) return SARA_OK;
+  if (!d_logits || !d_rid || !d_pos || !d_tok) return einval("null array");
+  if (!(temperature > 0.f)) return einval("temperature must be > 0");
+  if (!(top_p > 0.f && top_p <= 1.f)) return einval("top_p must be in (0, 1]");
+  if (eos_id >= vocab) return einval("eos_id out of range");
+  if (n_rows > SARA_NOALLOC_MAX_ROWS)
+    return einval("n_rows exceeds SARA_NOALLOC_MAX_ROWS (" + std::to_string(SARA_NOALLOC_MAX_ROWS) + ")");
+  if (top_p < 1.f && n_rows > SARA_NOALLOC_MAX_TOPP_ROWS)
+    return einval("n_rows exceeds SARA_NOALLOC_MAX_TOPP_ROWS (" + std::to_string(SARA_NOALLOC_MAX_TOPP_ROWS) +
+                  ") with top_p < 1");
+  int dev = -1;
+  HIP_TRY(hipGetDevice(&dev), "hipGetDevice");
+  if (stream) {
+    int sdev = -1;
+    HIP_TRY(hipStreamGetDevice((hipStream_t)stream, &sdev), "hipStreamGetDevice");
+    if (sdev != dev) return einval("stream belongs to another device than the current one");
+  }
+  return launch_sample_rows_noalloc(d_logits, n_rows, vocab, d_rid, d_pos, seed, step_index, temperature, top_p,
+                                    eos_id, forced_eos_u32, d_tok, (hipStream_t)stream);
+}
+
 extern "C" int sara_gumbel_fast_max_error(double* h_out, void* stream) {
   if (!h_out) return einval("h_out is null");
   return launch_gumbel_check(h_out, (hipStream_t)stream);

@@ -24,6 +24,10 @@ constexpr int kAttnTile = 64;        // tokens per LDS tile inside a split
 constexpr int kSampleChunks = 16;    // vocabulary chunks per sampled row
 constexpr int kTopPChunks = 16;      // vocabulary chunks per row in the top-p passes
 constexpr int kTopPBins = 2048;      // 11-bit digits of the top-p radix descent
+// static scratch of the allocation-free sampler (sara_sample_logits_noalloc)
+constexpr int kNoAllocMaxRows = SARA_NOALLOC_MAX_ROWS;
+constexpr int kNoAllocMaxToppRows = SARA_NOALLOC_MAX_TOPP_ROWS;
+constexpr size_t kNoAllocScratchBytes = SARA_NOALLOC_SCRATCH_BYTES;
 constexpr int kCtlThreads = 1024;    // threads of the single-workgroup controller
 constexpr int kMaxQueue = 4096;      // pending rollouts held in LDS by the refill
 constexpr int kMaxSlots = 4096;
@@ -230,6 +234,9 @@ int launch_grpo(const float* r, const int32_t* off, int n_groups, float eps, flo
 int launch_sample_rows(const float* logits, int n_rows, int V, const int32_t* rid,
                        const int32_t* pos, uint64_t seed, int step, float temp, float top_p, int eos,
                        uint32_t feos, int32_t* tok, hipStream_t st);
+int launch_sample_rows_noalloc(const float* logits, int n_rows, int V, const int32_t* rid, const int32_t* pos,
+                               uint64_t seed, int step, float temp, float top_p, int eos, uint32_t feos,
+                               int32_t* tok, hipStream_t st);
 int launch_convert_norms(sara_ctx* c, const void* const* w);
 int launch_gumbel_check(double* h_out, hipStream_t st);
 int launch_tile_weights(sara_ctx* c, const void* src, void* dst, int rows, int K, int tile_mul, int tile_add,
