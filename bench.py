@@ -116,6 +116,9 @@ def main():
                          "posterior-sampling queue priority")
     ap.add_argument("--top-p", type=float, default=1.0,
                     help="nucleus sampling mass (default 1: the full softmax, as every workload uses)")
+    ap.add_argument("--first-step", type=int, default=0,
+                    help="allocation-step index of the first pool (the long-rollout workload's success-rate "
+                         "mixture drifts with it); warm-up, timed and profiled steps take consecutive indices")
     ap.add_argument("--graph-iters", type=int, default=16)
     ap.add_argument("--chunk-iters", type=int, default=2048)
     ap.add_argument("--time-budget", type=float, default=60.0,
@@ -218,7 +221,7 @@ def main():
     n_pools = max(1, args.warmup) + max(1, args.steps) + 1
     pools = []
     for s in range(n_pools):
-        p = W.make_pool(cfg, s)
+        p = W.make_pool(cfg, args.first_step + s)
         d_tok = torch.from_numpy(p["tokens"]).cuda()
         d_p = torch.from_numpy(p["p"]).cuda()
         d_fl = torch.from_numpy(np.ascontiguousarray(p["forced_len"].reshape(-1))).cuda() \
@@ -275,7 +278,8 @@ def main():
         "warmup": n_warm, "ms_per_step": 1e3 * dt / n_steps, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": cfg["model"]["dtype"],
         "data": "synthetic (random-init weights, seeded prompt pools and success rates)",
-        "config": {"workload": describe(cfg)},
+        "config": {"workload": describe(cfg),
+                   "allocation_steps": [args.first_step + n_warm + i for i in range(n_steps)]},
         "steps_requested": args.steps, "warmup_requested": args.warmup,
         "time_budget_s": args.time_budget, "timed_s": dt,
         "effective_groups_per_s": committed / dt,

@@ -562,8 +562,8 @@ __device__ __forceinline__ void gemm_mblock(const uint16_t* __restrict__ X, cons
 // bf16 MFMA GEMM over tiled weights.  The live row count M is read on the
 // device; each m-block of up to 16*MTMAX rows runs the instance with just
 // enough 16-row tiles (ceil(rows / 16)), so small batches spend no MFMA,
-// LDS or X traffic on empty tiles.  Decode launches use grid z = 1 and loop
-// over the m-blocks; prefill launches one z block per m-block.
+// LDS or X traffic on empty tiles.  Launches have one z block per m-block of
+// the row capacity; z blocks past the live rows exit after reading M.
 // PF only separates the prefill instances from the decode ones in profiles.
 template <int NT, int MTMAX, int KC, int EPI, int PF>
 __global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __restrict__ X,
@@ -1990,8 +1990,10 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     const bool two = wide || (K >= 4096 && c->in_prefill);
     const int rows_per_block = two ? 128 : 64;
     int tiles_n = (N + rows_per_block - 1) / rows_per_block;
-    // decode: one z block loops over the live m-blocks; prefill: exact m-blocks
-    int zb = c->in_prefill ? (M_cap + 16 * MT - 1) / (16 * MT) : 1;
+    // one z block per m-block of the capacity; in decode the live row count
+    // is read on the device, and z blocks past it exit at once (blocks are
+    // dispatched z-major, so the live m-blocks start first)
+    int zb = (M_cap + 16 * MT - 1) / (16 * MT);
     int want = (tiles_n >= 256) ? 1 : (256 + tiles_n - 1) / tiles_n;
     // 64-wide k chunks: four pipeline slots of X + W fit in registers for NT <= 2
     const int KC = 64;
@@ -2053,7 +2055,7 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
 static void gemm_swiglu(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr, int M_cap) {
   constexpr int MT = 8;
   const int N = 2 * c->ffn, K = c->d;
-  dim3 grid((N + 127) / 128, 1, c->in_prefill ? (M_cap + 16 * MT - 1) / (16 * MT) : 1);
+  dim3 grid((N + 127) / 128, 1, (M_cap + 16 * MT - 1) / (16 * MT));
   if (c->in_prefill)
     launch_k(c, c->stream, (k_gemm_bf16_lds<2, MT, 64, 1, 1>), grid, dim3(256), 0, (const uint16_t*)X,
                        (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0, SampleArgs{});
