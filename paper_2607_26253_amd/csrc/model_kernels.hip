@@ -1297,7 +1297,8 @@ __global__ __launch_bounds__(256) void k_qkv_rope(const uint16_t* __restrict__ X
     uint16_t* __restrict__ qbuf, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
   __shared__ f32x4 red[4][8][64];
   const int M = *M_ptr;
-  for (int m_base = 0; m_base < M; m_base += 128) {
+  // one z block per 128-row m-block of the capacity (those past M exit)
+  for (int m_base = blockIdx.z * 128; m_base < M; m_base += gridDim.z * 128) {
     const int mt = min(8, (M - m_base + 15) >> 4);
     // depth: every k step (at most 16) in flight for up to 32 rows, then a half and a quarter
 #define SARA_QR(MT_, D_) \
@@ -2107,7 +2108,8 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
       // paged attention, then the merge of rows with several context splits
       PROF_B(c);
 #define SARA_QKV(KS_) \
-      launch_k(c, st, (k_qkv_rope<HD, KS_>), dim3(c->nqkv / 16), dim3(256), 0, (const uint16_t*)x, \
+      launch_k(c, st, (k_qkv_rope<HD, KS_>), dim3(c->nqkv / 16, 1, (M_cap + 127) / 128), dim3(256), 0, \
+               (const uint16_t*)x, \
                          (const uint16_t*)c->w_qkv[l], M_ptr, d, c->rows, c->row_rope, c->hq, c->hkv, l, \
                          c->n_blocks, (uint16_t*)c->qbuf, (uint16_t*)c->kc, (uint16_t*)c->vc)
       switch (d / 128) {
@@ -2298,7 +2300,7 @@ int launch_decode(sara_ctx* c, const int32_t* forced, float* logits, int model_f
       // nucleus sampler, whose winner replaces the epilogue's
       float* lg_out = (c->topp && !logits) ? c->topp_logits : logits;
       PROF_B(c);
-      launch_k(c, st, (k_gemm_bf16_lds<2, 8, 64, 2, 0>), dim3(nb, 1, 1), dim3(256), 0,
+      launch_k(c, st, (k_gemm_bf16_lds<2, 8, 64, 2, 0>), dim3(nb, 1, (S + 127) / 128), dim3(256), 0,
                          (const uint16_t*)c->x, (const uint16_t*)c->lm_head, (void*)nullptr, c->rows_M, c->V,
                          c->d, c->d, (int64_t)0,
                          SampleArgs{c->rows, (const CtlParams*)c->cp_dev, lg_out, c->samp_best, c->samp_idx, S});
