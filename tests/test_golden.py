@@ -24,3 +24,10 @@ def test_abandon_time_table():
         while P.decide(n, 0, 8, 8, float(tau))[0] == P.CONTINUE:
             n += 1
         assert n == int(n_a)
+
+
+def test_ablation_table_is_the_oracles():
+    """tests/golden/ablation_sweeps.txt is exactly what the committed oracle
+    writes for the ablation sweeps (the GPU test compares against it)."""
+    from tests.golden import make_ablation_table as AB
+    assert AB.oracle_lines() == AB.read_golden()

@@ -1,5 +1,8 @@
-"""Full-size parity on the Qwen2.5-1.5B-shaped workload in the launch
-configuration bench.py times (HIP-graph replay, 512 slots, 1024 new tokens).
+"""Full-size parity in the launch configuration bench.py times (HIP-graph
+replay, full slot pools and generation lengths): the Qwen2.5-1.5B-shaped
+workload (512 slots, 1024 new tokens), the 3B-shaped one (36 layers, forced
+EOS 1/800, up to 2048 new tokens) and the long-rollout one at the last step
+of its drift (256 binding slots, lognormal forced lengths up to 4096).
 
 The oracle cannot generate a full step, so it checks what it can compute
 one by one or what holds at any size:
@@ -9,7 +12,8 @@ one by one or what holds at any size:
 * reward: the oracle's hash chain over each rollout's GPU tokens gives the
   GPU's reward;
 * GRPO advantages of the committed groups;
-* tokens: at sampled positions of sampled rollouts, the oracle's own logits
+* tokens: at sampled positions (within a rollout's first 384 tokens, which
+  bounds the oracle's forward) of sampled rollouts, the oracle's own logits
   (one teacher-forced forward over the GPU's tokens) and sampler give the
   GPU's token (bf16 rounding noise flips a near tie now and then, so >= 90%
   agreement is required);
@@ -28,13 +32,19 @@ from tests.gpu_harness import compare_logs, device_setup, run_gpu_step
 pytestmark = pytest.mark.gpu
 
 
-def test_full_size_qwen1p5b_step():
+POSITION_CAP = 384
+
+
+@pytest.mark.parametrize("name,step", [("qwen1p5b_shape", 0), ("qwen3b_shape", 0), ("long_ragged_1p5b", 299)])
+def test_full_size_step(name, step):
     import torch
     assert torch.cuda.is_available()
-    cfg = W.get_config("qwen1p5b_shape")
+    cfg = W.get_config(name)
     a, m = cfg["alloc"], cfg["model"]
     k, U = a["k"], a["pool_U"]
-    pool = W.make_pool(cfg, 0)
+    pool = W.make_pool(cfg, step)
+    print(f"[full] {name} step {step}: {m['n_layers']} layers, {a['n_slots']} slots, max_new {a['max_new']}",
+          flush=True)
     seed = W.sampling_seed(cfg)
     ctx, w = device_setup(cfg)
     print("[full] running the GPU step (graph replay)", flush=True)
@@ -47,7 +57,7 @@ def test_full_size_qwen1p5b_step():
     outcome = {(int(u), int(j)): (int(L), int(r)) for (t, s, u, j, L, r) in fin}
 
     # controller replay
-    ora = OC.simulate(a, U, lambda pairs: [outcome[p] for p in pairs])
+    ora = OC.simulate(a, U, lambda pairs: [outcome[p] for p in pairs], draw_key=(seed, pool["step"]))
     compare_logs(gpu["logs"], ora)
     assert (st["committed"], st["rollouts"], st["tokens"], st["decode_steps"], st["budget_left"]) == (
         ora["n_committed"], ora["rollouts"], ora["tokens"], ora["decode_steps"], ora["budget_left"])
@@ -83,7 +93,8 @@ def test_full_size_qwen1p5b_step():
         prompt = pool["tokens"][pool["offsets"][u]:pool["offsets"][u + 1]]
         P = len(prompt)
         gen = ro["tokens"][u * k + j][:L]
-        pos = sorted(set([0, L - 1] + list(g.choice(L, size=6, replace=False))))
+        Lc = min(L, POSITION_CAP)
+        pos = sorted(set([0, Lc - 1] + list(g.choice(Lc, size=min(6, Lc), replace=False))))
         seq = np.concatenate([prompt, gen[:max(pos)]])
         cache = dec.new_cache(len(seq))
         logits = dec.forward(seq, np.arange(len(seq)), cache, logit_rows=[P - 1 + i for i in pos])

@@ -513,70 +513,65 @@ def test_tiny_allocation_edges(torch_cuda, over):
 
 def test_ablation_sweeps_with_exact_counterfactuals(torch_cuda):
     """The tau, n0 and k ablations on the device, with exact counterfactual
-    labels (section 8(f): sweeps, lost groups, decision quality).
-    Model-free rollouts of equal length over a 2048-prompt pool of the
-    success-rate mixture; for every k the fixed-k run on the same token table
-    labels each drawn prompt with its full group (its first n rewards are
-    SARA's, by the logical rollout keys).  Checked at every point: each
+    labels (mechanism and ablation figures: sweeps, lost groups, decision
+    quality, Fig. 3a and 3c analogs).  Model-free rollouts of equal length
+    over a 2048-prompt pool of the success-rate mixture; for every k the
+    fixed-k run on the same token table labels each drawn prompt with its
+    full group (its first n rewards are SARA's, by the logical rollout keys).
+    At every point: the GPU's decision, draw, assignment and finish logs equal
+    the oracle's; the table rows computed from the GPU's results equal the
+    oracle-written golden file tests/golden/ablation_sweeps.txt; each
     abandonment happens at n_stop = max(n0, k - floor(tau (k+1))) on an
-    all-same prefix, each commit at n = k on a mixed one, and the rollouts
+    all-same prefix and each commit at n = k on a mixed one; and the rollouts
     per drawn prompt match sum_u [n_stop + (k - n_stop) q_u],
     q_u = 1 - p_u^n_stop - (1-p_u)^n_stop, within 5 sigma."""
-    full = W.get_config("tiny_f32")
-    base = W.get_config("tiny_f32")
-    base["alloc"].update(B=10 ** 6, budget_N=2048, pool_U=2048, n_slots=512, max_new=4)
-    base["model"]["eos_id"] = -1
-    w = W.make_weights(full)
-    labels = {}
+    from tests.golden import make_ablation_table as AB
+    w = W.make_weights(W.get_config("tiny_f32"))
+    golden = AB.read_golden()
+    labels, label_runs = {}, {}
 
-    def point(k, n0, tau):
-        cfg = dict(base, alloc=dict(base["alloc"], k=k, n0=n0, commit_min=k, tau_low=tau))
+    def gpu_run(cfg):
         pool = W.make_pool(cfg, 0)
-        p = pool["p"]
-        tab = _model_free_case(cfg, 5)
-        if k not in labels:
-            fk = W.fixed_k_variant(cfg)
-            fk["alloc"]["budget_N"] = 4096
-            ctx, _ = device_setup(fk, w)
-            labels[k] = run_gpu_step(ctx, fk, pool, forced=tab, model_free=True)
-            ctx.close()
-        lab = labels[k]
-        rf = lab["roll"]
         ctx, _ = device_setup(cfg, w)
-        g = run_gpu_step(ctx, cfg, pool, forced=tab, model_free=True)
+        g = run_gpu_step(ctx, cfg, pool, forced=AB.token_table(cfg), model_free=True)
         ctx.close()
-        rs, st = g["roll"], g["stats"]
-        drawn = st["drawn"]
-        assert lab["stats"]["drawn"] >= drawn
-        n_stop = max(n0, min(k, k - math.floor(tau * (k + 1))))
-        lost, want, var = 0, 0.0, 0.0
-        for u in range(drawn):
-            n, s = int(rs["n"][u]), int(rs["s"][u])
-            assert np.array_equal(rs["reward"][u * k:u * k + n], rf["reward"][u * k:u * k + n])
-            s_full = int(np.sum(rf["reward"][u * k:(u + 1) * k]))
-            if rs["status"][u] == 2:
-                assert n == k and 1 <= s <= k - 1
-            else:
-                assert rs["status"][u] == 3 and n == n_stop and s in (0, n)
-                lost += int(1 <= s_full <= k - 1)
-            q = 1 - p[u] ** n_stop - (1 - p[u]) ** n_stop
-            want += n_stop + (k - n_stop) * q
-            var += (k - n_stop) ** 2 * q * (1 - q)
-        assert abs(st["rollouts"] - want) <= 5 * math.sqrt(var) + 1e-9
-        ab = drawn - st["committed"]
-        return (k, n0, tau, n_stop, drawn, st["rollouts"] / drawn, st["rollouts"] / max(st["committed"], 1),
-                st["committed"], 100.0 * lost / max(ab, 1), 100.0 * (1 - lost / drawn), st["decode_steps"])
+        ora, _ = AB.oracle_run(cfg)
+        compare_logs(g["logs"], ora)
+        st, rs = g["stats"], g["roll"]
+        return g, dict(drawn=st["drawn"], rollouts=st["rollouts"], committed=st["committed"],
+                       decode_steps=st["decode_steps"], status=rs["status"], n=rs["n"], reward=rs["reward"],
+                       decisions=g["logs"]["decisions"][:, :5], assigns=g["logs"]["assigns"]), pool
 
-    rows = [point(8, 2, tau) for tau in (0.1, 0.3, 0.45, 0.6)]
-    rows += [point(8, n0, 0.45) for n0 in (1, 4)]
-    rows += [point(k, 2, 0.45) for k in (4, 16)]
-    print("[sweep] k n0 tau n_stop drawn rollouts/drawn rollouts/effective committed lost% quality% "
-          "decode_steps", flush=True)
-    for r in rows:
-        print("[sweep] %d %d %.2f %d %d %.3f %.2f %d %.1f %.1f %d" % r, flush=True)
-    # a higher threshold abandons sooner: fewer rollouts per drawn prompt
-    per = [r[5] for r in rows[:4]]
-    assert all(a > b for a, b in zip(per, per[1:]))
+    lines = []
+    for (k, n0, tau) in AB.POINTS:
+        if k not in labels:
+            _, lab, _ = gpu_run(AB.label_config(k))
+            labels[k], label_runs[k] = lab["reward"], lab
+        cfg = AB.point_config(k, n0, tau)
+        g, run, pool = gpu_run(cfg)
+        p = pool["p"]
+        st, rs = g["stats"], g["roll"]
+        assert label_runs[k]["drawn"] >= st["drawn"]
+        ns = AB.n_stop(k, n0, tau)
+        want, var = 0.0, 0.0
+        for u in range(st["drawn"]):
+            n, s_ = int(rs["n"][u]), int(rs["s"][u])
+            assert np.array_equal(rs["reward"][u * k:u * k + n], labels[k][u * k:u * k + n])
+            if rs["status"][u] == 2:
+                assert n == k and 1 <= s_ <= k - 1
+            else:
+                assert rs["status"][u] == 3 and n == ns and s_ in (0, n)
+            q = 1 - p[u] ** ns - (1 - p[u]) ** ns
+            want += ns + (k - ns) * q
+            var += (k - ns) ** 2 * q * (1 - q)
+        assert abs(st["rollouts"] - want) <= 5 * math.sqrt(var) + 1e-9
+        lines += AB.summarize(k, n0, tau, run, labels[k])
+        if (k, n0, tau) == AB.DEFAULT:
+            lines.append(AB.fig3c("sara", k, run))
+            lines.append(AB.fig3c("fixed_k", k, label_runs[k]))
+    for l in lines:
+        print("[sweep]", l, flush=True)
+    assert lines == golden
 
 
 @pytest.mark.parametrize("variant", ["warm_start", "thompson"])
