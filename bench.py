@@ -34,7 +34,7 @@ import workloads as W  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
 BF16_PEAK_TFLOPS = 2500.0
-TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_decode_qwen1p5b_shape_128rows.md")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_decode_qwen1p5b_shape_32rows.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_26253_amd", "csrc", "model_kernels.hip")
 
 
@@ -55,7 +55,7 @@ def measured_traffic(kernel):
         cells = [c.strip() for c in line.strip().strip("|").split("|")]
         if len(cells) == 7 and cells[0] == f"`{kernel}`" and cells[5] != "-":
             return {"traffic": float(cells[4]), "alg_bytes_per_launch": float(cells[5]), "ratio": float(cells[6]),
-                    "regime": "16 eager decode iterations at 128 rows (first allocation step)",
+                    "regime": "16 eager decode iterations at 32 rows (start of allocation step 0, goal B = 16)",
                     "source": os.path.relpath(TRAFFIC_PROFILE, ROOT)}
     return None
 
@@ -136,6 +136,9 @@ def main():
                     help="counter mode: run this many eager decode/decide/refill iterations of step 0 with "
                          "per-kernel event profiling and print each kernel class's algorithmic bytes per "
                          "launch (pair it with rocprofv3 --pmc over the same run), then exit")
+    ap.add_argument("--counter-rows", type=int, default=0,
+                    help="counter mode: goal B = rows / n0, so the first decode iterations run about this "
+                         "many rows (default: the workload's B)")
     ap.add_argument("--decode-iters", type=int, default=0,
                     help="profiling mode: only replay this many decode/decide/refill iterations of "
                          "step 0 from the HIP graph (for kernel traces), then exit")
@@ -160,6 +163,8 @@ def main():
         cfg["alloc"]["mode"] = "sara_thompson"
     if args.top_p != 1.0:
         cfg["alloc"]["top_p"] = args.top_p
+    if args.counter_pass and args.counter_rows:
+        cfg["alloc"]["B"] = max(1, args.counter_rows // cfg["alloc"]["n0"])
     t0 = time.time()
     weights = W.make_weights(cfg)
     t_w = time.time() - t0
@@ -350,7 +355,8 @@ def main():
             "decode_hbm_frac": tot_by / (tot_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "classes": {k["name"]: {"launches": k["launches"], "ms": round(k["ms"], 3),
                                     "avg_us": round(1e3 * k["ms"] / k["launches"], 2),
-                                    "GBps": round(k["bytes"] / (k["ms"] * 1e-3) / 1e9, 1) if k["ms"] else None}
+                                    "GBps": round(k["bytes"] / (k["ms"] * 1e-3) / 1e9, 1) if k["ms"] else None,
+                                    "TFLOPs": round(k["flops"] / (k["ms"] * 1e-3) / 1e12, 1) if k["ms"] else None}
                         for k in allc},
             "wall_s": tprof,
         }

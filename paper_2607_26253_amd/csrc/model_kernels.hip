@@ -564,7 +564,8 @@ __device__ __forceinline__ void gemm_mblock(const uint16_t* __restrict__ X, cons
 // enough 16-row tiles (ceil(rows / 16)), so small batches spend no MFMA,
 // LDS or X traffic on empty tiles.  Launches have one z block per m-block of
 // the row capacity; z blocks past the live rows exit after reading M.
-// PF only separates the prefill instances from the decode ones in profiles.
+// PF only labels the instance in profiles: 0 decode, 1 prefill, 2 the decode
+// attention-output projection (so every decode weight matrix has a class).
 template <int NT, int MTMAX, int KC, int EPI, int PF>
 __global__ __launch_bounds__(256, 2) void k_gemm_bf16_lds(const uint16_t* __restrict__ X,
     const uint16_t* __restrict__ W, void* __restrict__ out, const int32_t* __restrict__ M_ptr,
@@ -1979,7 +1980,7 @@ static void launch_k(sara_ctx* c, hipStream_t st, F kernel, dim3 grid, dim3 bloc
   }
 }
 static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr, int M_cap,
-                int N, int K, int& splits_out, int max_splits = 1 << 30) {
+                int N, int K, int& splits_out, int max_splits = 1 << 30, bool oproj = false) {
   int64_t stride = (int64_t)M_cap * N;
   if (c->md.dtype == SARA_BF16) {
     // weight rows per block: 128 (two 16-row tiles per wave) for the LM head
@@ -2024,9 +2025,12 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     if (c->in_prefill) {
       if (two) SARA_GEMM(2, 64, 1);
       else SARA_GEMM(1, 64, 1);
+    } else if (two) {
+      SARA_GEMM(2, 64, 0);
+    } else if (oproj) {
+      SARA_GEMM(1, 64, 2);
     } else {
-      if (two) SARA_GEMM(2, 64, 0);
-      else SARA_GEMM(1, 64, 0);
+      SARA_GEMM(1, 64, 0);
     }
 #undef SARA_GEMM
     splits_out = splits;
@@ -2171,8 +2175,8 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
     PROF_E(c, kPCombine, 0, 0);
     }
     PROF_B(c);
-    gemm(c, x, c->w_o[l], M_ptr, M_cap, d, c->qdim, sp);
-    PROF_E(c, kPGemmN1, d, c->qdim);
+    gemm(c, x, c->w_o[l], M_ptr, M_cap, d, c->qdim, sp, 1 << 30, true);
+    PROF_E(c, (c->md.dtype == SARA_BF16 && !c->in_prefill) ? kPGemmO1 : kPGemmN1, d, c->qdim);
     PROF_B(c);
     residual_norm<T>(c, M_ptr, M_cap, sp, c->norms + (size_t)(2 * l + 1) * d);
     PROF_E(c, kPResNorm, d, 0);

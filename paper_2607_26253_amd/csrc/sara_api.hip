@@ -37,7 +37,7 @@ const char* const kProfNames[kPNumClasses] = {
     "k_gemm_bf16_lds<1,8,64,0,0>", "k_gemm_bf16_lds<2,8,64,1,0>", "k_gemm_bf16_lds<2,8,64,2,0>",
     "k_attn_dec<128>", "k_attn_combine", "k_qkv_epilogue", "k_residual_norm_v", "k_swiglu",
     "k_embed_norm", "k_sample_partial", "k_sample_final", "k_decode_rows", "k_copy_logits", "k_qkv_rope",
-    "k_topp_max", "k_topp_hist", "k_topp_pick",
+    "k_topp_max", "k_topp_hist", "k_topp_pick", "k_gemm_bf16_lds<1,8,64,0,2>",
     ".gemm[q|k|v]", ".gemm[o]", ".gemm[gate|up]", ".gemm[down]", ".gemm[lm_head]"};
 
 // prof_begin reserves an event pair for the next kernel launch; launch_k
@@ -75,6 +75,7 @@ int prof_collect(sara_ctx* c) {
     double by = 0.0, fl = 0.0, N = r.N, K = r.K;
     switch (r.cls) {
       case kPGemmN1:
+      case kPGemmO1:
         by = N * K * E + m * K * E + m * N * 4.0; fl = 2.0 * m * N * K; break;
       case kPGemmLM:   // bf16: sampling epilogue, one (score, id) per row and 128-id block
         by = N * K * E + m * K * E + (E == 2 ? m * ((N + 127) / 128) * 8.0 : m * N * 4.0);
@@ -108,7 +109,7 @@ int prof_collect(sara_ctx* c) {
       t.flops += fl;
     };
     add(r.cls);
-    if (r.cls == kPGemmN1 || r.cls == kPGemmGU || r.cls == kPGemmLM || r.cls == kPQkvRope) {
+    if (r.cls == kPGemmN1 || r.cls == kPGemmO1 || r.cls == kPGemmGU || r.cls == kPGemmLM || r.cls == kPQkvRope) {
       if (r.N == c->V) add(kPGemmLm);
       else if (r.N == c->nqkv) add(kPGemmQkv);
       else if (r.N == 2 * c->ffn) add(kPGemmGu);

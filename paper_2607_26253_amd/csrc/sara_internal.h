@@ -207,7 +207,7 @@ namespace sara {
 // trace names them), then a breakdown of the GEMMs by weight matrix
 enum ProfClass { kPGemmN1, kPGemmGU, kPGemmLM, kPAttn, kPCombine, kPQkv, kPResNorm, kPSwiglu,
                  kPEmbed, kPSampleP, kPSampleF, kPRows, kPCopy, kPQkvRope, kPToppMax, kPToppHist, kPToppSel,
-                 kPGemmQkv, kPGemmO, kPGemmGu, kPGemmD, kPGemmLm, kPNumClasses };
+                 kPGemmO1, kPGemmQkv, kPGemmO, kPGemmGu, kPGemmD, kPGemmLm, kPNumClasses };
 extern const char* const kProfNames[kPNumClasses];
 void prof_begin(sara_ctx* c);
 void prof_end(sara_ctx* c, int cls, int N = 0, int K = 0);
