@@ -195,7 +195,9 @@ def main():
         print(json.dumps({"mode": "counter_pass", "workload": describe(cfg), "iters": args.counter_pass,
                           "running_slots": q["running"],
                           "classes": {k["name"]: {"launches": k["launches"],
-                                                  "alg_bytes_per_launch": k["bytes"] / k["launches"]}
+                                                  "alg_bytes_per_launch": k["bytes"] / k["launches"],
+                                                  "alg_flops_per_launch": k["flops"] / k["launches"],
+                                                  "event_us": 1e3 * k["ms"] / k["launches"]}
                                       for k in prof if k["launches"] > 0}}), flush=True)
         ctx.close()
         return
