@@ -841,6 +841,64 @@ __global__ __launch_bounds__(256) void k_residual_norm_v(const int32_t* __restri
 
 // a = silu(g) * u from the fused gate|up output ([m][2*ffn]); grid-stride
 // over the M * ffn outputs of the live rows
+// bf16 decode variant of the residual norm: one row per block, one float4
+// of the row per thread (blockDim = d/4 rounded up to whole waves).  The
+// residual, the norm weight and the row's split-K partials of that float4
+// (only the splits the GEMM wrote) are loaded at once, summed in split order
+// into four interleaved accumulators, and the row's sum of squares is
+// reduced over the block's waves in wave order; x receives four bf16 per
+// thread in one 8-byte store (row-major, or fragment-major for the q|k|v
+// kernel, where four consecutive k of a row are contiguous).
+__global__ __launch_bounds__(1024) void k_residual_norm_f4(const int32_t* __restrict__ M_ptr,
+    const float* __restrict__ ws, int splits, int64_t stride, int d, float* __restrict__ h,
+    const float* __restrict__ w, float eps, uint16_t* __restrict__ x, int x_tiled) {
+  __shared__ float red[16];
+  const int M = *M_ptr;
+  const int nq = d >> 2, q = threadIdx.x, lane = q & 63, wave = q >> 6;
+  const int nw = (blockDim.x + 63) >> 6;
+  const bool on = q < nq;
+  const int qc = on ? q : nq - 1;
+  for (int i = blockIdx.x; i < M; i += gridDim.x) {
+    const size_t rb = (size_t)i * d;
+    const float4 hv = ((const float4*)(h + rb))[qc];
+    const float4 wv = ((const float4*)w)[qc];
+    float4 p[kMaxSplitsDec];
+#pragma unroll
+    for (int sp = 0; sp < kMaxSplitsDec; ++sp)
+      p[sp] = (sp < splits) ? ((const float4*)(ws + (size_t)sp * stride + rb))[qc] : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 a[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) a[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int sp = 0; sp < kMaxSplitsDec; ++sp) {
+      a[sp & 3].x += p[sp].x; a[sp & 3].y += p[sp].y; a[sp & 3].z += p[sp].z; a[sp & 3].w += p[sp].w;
+    }
+    float4 v;
+    v.x = hv.x + ((a[0].x + a[1].x) + (a[2].x + a[3].x));
+    v.y = hv.y + ((a[0].y + a[1].y) + (a[2].y + a[3].y));
+    v.z = hv.z + ((a[0].z + a[1].z) + (a[2].z + a[3].z));
+    v.w = hv.w + ((a[0].w + a[1].w) + (a[2].w + a[3].w));
+    float ss = 0.f;
+    if (on) {
+      ((float4*)(h + rb))[q] = v;
+      ss = (v.x * v.x + v.y * v.y) + (v.z * v.z + v.w * v.w);
+    }
+    ss = wave_sum(ss);
+    if (lane == 0) red[wave] = ss;
+    __syncthreads();
+    float tot = 0.f;
+    for (int k = 0; k < nw; ++k) tot += red[k];
+    const float inv = 1.0f / sqrtf(tot / (float)d + eps);
+    if (on) {
+      const uint32_t lo = (uint32_t)f32_to_bf16(v.x * inv * wv.x) | ((uint32_t)f32_to_bf16(v.y * inv * wv.y) << 16);
+      const uint32_t hi = (uint32_t)f32_to_bf16(v.z * inv * wv.z) | ((uint32_t)f32_to_bf16(v.w * inv * wv.w) << 16);
+      const size_t o = x_tiled ? (size_t)tiled_index(i, 4 * q, d) : rb + 4 * q;
+      *(uint2*)(x + o) = make_uint2(lo, hi);
+    }
+    __syncthreads();   // red[] is reused by the next row
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void k_swiglu(const int32_t* __restrict__ M_ptr,
     const float* __restrict__ ws, int splits, int64_t stride, int ffn, T* __restrict__ a) {
@@ -2082,6 +2140,11 @@ static void residual_norm(sara_ctx* c, const int32_t* M_ptr, int M_cap, int sp, 
   const dim3 grid(std::min(M_cap, 1024));
   const int64_t stride = (int64_t)M_cap * d;
   T* x = (T*)c->x;
+  if (sizeof(T) == 2 && !c->in_prefill && sp <= kMaxSplitsDec && d % 4 == 0 && d / 4 <= 1024) {
+    launch_k(c, c->stream, k_residual_norm_f4, grid, dim3((d / 4 + 63) / 64 * 64), 0, M_ptr, c->ws, sp, stride,
+             d, c->h, w, c->md.rms_eps, (uint16_t*)c->x, x_tiled);
+    return;
+  }
 #define SARA_RN(V) launch_k(c, c->stream, (k_residual_norm_v<T, V>), grid, dim3(256), 0, M_ptr, c->ws, \
                                       sp, stride, d, c->h, w, c->md.rms_eps, x, x_tiled)
   switch (sp <= kMaxSplitsDec ? vpt : 0) {

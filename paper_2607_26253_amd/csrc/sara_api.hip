@@ -35,7 +35,7 @@ static int einval(const std::string& msg) {
 
 const char* const kProfNames[kPNumClasses] = {
     "k_gemm_bf16_lds<1,8,64,0,0>", "k_gemm_bf16_lds<2,8,64,1,0>", "k_gemm_bf16_lds<2,8,64,2,0>",
-    "k_attn_dec<128>", "k_attn_combine", "k_qkv_epilogue", "k_residual_norm_v", "k_swiglu",
+    "k_attn_dec<128>", "k_attn_combine", "k_qkv_epilogue", "k_residual_norm_f4", "k_swiglu",
     "k_embed_norm", "k_sample_partial", "k_sample_final", "k_decode_rows", "k_copy_logits", "k_qkv_rope",
     "k_topp_max", "k_topp_hist", "k_topp_pick", "k_gemm_bf16_lds<1,8,64,0,2>",
     ".gemm[q|k|v]", ".gemm[o]", ".gemm[gate|up]", ".gemm[down]", ".gemm[lm_head]"};
