@@ -2054,7 +2054,11 @@ static int gemm(sara_ctx* c, const void* X, const void* W, const int32_t* M_ptr,
     // is read on the device, and z blocks past it exit at once (blocks are
     // dispatched z-major, so the live m-blocks start first)
     int zb = (M_cap + 16 * MT - 1) / (16 * MT);
-    int want = (tiles_n >= 256) ? 1 : (256 + tiles_n - 1) / tiles_n;
+    // blocks without a split: weight tiles x m-blocks in prefill (the chunk's
+    // row count is known), weight tiles alone in decode (live rows are few
+    // and known only on the device)
+    const int64_t blocks = (int64_t)tiles_n * (c->in_prefill ? zb : 1);
+    int want = (blocks >= 256) ? 1 : (int)((256 + blocks - 1) / blocks);
     // 64-wide k chunks: four pipeline slots of X + W fit in registers for NT <= 2
     const int KC = 64;
     int chunks = K / KC;

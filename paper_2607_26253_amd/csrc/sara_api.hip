@@ -229,9 +229,22 @@ extern "C" int sara_init(const sara_model_desc* md, const sara_alloc_desc* ad,
                                 (c->MAXB + kAttnChunks - 1) / kAttnChunks);
   c->dec_splits_max = (c->MAXB + kDecPages - 1) / kDecPages;
   {
-    int64_t nd = std::max<int64_t>({c->V, c->nqkv, 2 * (int64_t)c->ffn, c->d});
-    int64_t np = std::max<int64_t>({c->nqkv, 2 * (int64_t)c->ffn, c->d});
-    c->ws_floats = std::max<int64_t>((int64_t)c->S * nd, (int64_t)c->prefill_rows * np);
+    // split-K partials of the VALU / MFMA GEMMs that write fp32 (the GEMM
+    // falls back to one split when its partials would not fit)
+    if (md->dtype == SARA_BF16) {
+      // decode: the o and down projections (<= kMaxSplitsDec splits of
+      // [S][d]); prefill: q|k|v, o and down over a chunk, whose weight tiles
+      // and m-blocks fill the GPU without splits except in a short last
+      // chunk (<= 256 blocks' worth of partials).  The LM head, the gate|up
+      // projection and the q|k|v projection of decode write no partials.
+      const int64_t npf = std::max<int64_t>(c->nqkv, c->d);
+      c->ws_floats = std::max<int64_t>((int64_t)kMaxSplitsDec * c->S * c->d, 2 * (int64_t)c->prefill_rows * npf);
+    } else {
+      // fp32: also the logits [S][V] and the gate|up output [rows][2 ffn]
+      int64_t nd = std::max<int64_t>({c->V, c->nqkv, 2 * (int64_t)c->ffn, c->d});
+      int64_t np = std::max<int64_t>({c->nqkv, 2 * (int64_t)c->ffn, c->d});
+      c->ws_floats = std::max<int64_t>((int64_t)c->S * nd, (int64_t)c->prefill_rows * np);
+    }
   }
   const size_t E = (size_t)c->elt;
   const size_t d = c->d;
