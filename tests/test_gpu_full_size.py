@@ -17,6 +17,10 @@ one by one or what holds at any size:
   (one teacher-forced forward over the GPU's tokens) and sampler give the
   GPU's token (bf16 rounding noise flips a near tie now and then, so >= 90%
   agreement is required);
+* logits: the step replayed eagerly for its first decode steps, teacher
+  forced with the GPU's own tokens, in the same launch configuration (full
+  slot pool, full depth): every row of three sampled rollouts within the
+  full-depth bounds of the bf16 slices against the oracle's forward;
 * invariants: budget, lengths, committed groups mixed, token count."""
 import numpy as np
 import pytest
@@ -27,12 +31,14 @@ from oracle import grpo as OG
 from oracle import reward as OR
 from oracle import sampler as OS
 from oracle.model import Decoder
-from tests.gpu_harness import compare_logs, device_setup, run_gpu_step
+from tests.gpu_harness import compare_logs, device_setup, forced_table, run_gpu_step
+from tests.test_gpu_bf16_slices import FULL_DEPTH_MAX_REL
 
 pytestmark = pytest.mark.gpu
 
 
 POSITION_CAP = 384
+LOGIT_STEPS = 4
 
 
 @pytest.mark.parametrize("name,step", [("qwen1p5b_shape", 0), ("qwen3b_shape", 0), ("long_ragged_1p5b", 299)])
@@ -49,6 +55,12 @@ def test_full_size_step(name, step):
     ctx, w = device_setup(cfg)
     print("[full] running the GPU step (graph replay)", flush=True)
     gpu = run_gpu_step(ctx, cfg, pool, use_graph=True)
+    # the same step again, eager and teacher forced with the GPU's own tokens,
+    # for its first decode steps with the logits captured
+    tf = forced_table(cfg, {(u, j): dict(tokens=gpu["roll"]["tokens"][u * k + j][:L])
+                            for (t_, s_, u, j, L, r_) in gpu["logs"]["finishes"]})
+    print(f"[full] teacher-forced eager replay of the first {LOGIT_STEPS} decode steps", flush=True)
+    tfr = run_gpu_step(ctx, cfg, pool, forced=tf, capture_logits=True, max_steps=LOGIT_STEPS)
     ctx.close()
     st = gpu["stats"]
     print(f"[full] GPU: {st['rollouts']} rollouts, {st['tokens']} tokens, {st['committed']} committed, "
@@ -107,3 +119,35 @@ def test_full_size_step(name, step):
         print(f"[full] rollout ({u},{j}) L={L}: checked positions {pos}", flush=True)
     print(f"[full] sampled-position agreement {agree}/{total}", flush=True)
     assert agree >= 0.9 * total
+
+    # logits of the teacher-forced replay: rows (decode step t, slot) of
+    # three rollouts started at the first decode step, against the oracle's
+    # forward over the same tokens (the oracle's own fp32-vs-fp64 spread,
+    # printed beside, on the first of them)
+    assert np.array_equal(tfr["logs"]["assigns"][:len(tfr["logs"]["assigns"])],
+                          gpu["logs"]["assigns"][:len(tfr["logs"]["assigns"])])
+    first = [(int(s_), int(u), int(j)) for (t0, s_, u, j) in tfr["logs"]["assigns"] if t0 == 0]
+    chosen = [first[i] for i in g.choice(len(first), size=3, replace=False)]
+    dec64 = Decoder(m, w, gemm_acc="f64")
+    worst, worst_rms, floor = 0.0, 0.0, 0.0
+    for c, (slot, u, j) in enumerate(chosen):
+        L = outcome[(u, j)][0]
+        n = min(LOGIT_STEPS, L)
+        prompt = pool["tokens"][pool["offsets"][u]:pool["offsets"][u + 1]]
+        P = len(prompt)
+        seq = np.concatenate([prompt, ro["tokens"][u * k + j][:n - 1]])
+        rows = [P - 1 + i for i in range(n)]
+        lo = dec.forward(seq, np.arange(len(seq)), dec.new_cache(len(seq)), logit_rows=rows)
+        lo64 = dec64.forward(seq, np.arange(len(seq)), dec64.new_cache(len(seq)), logit_rows=rows) if c == 0 else None
+        for i in range(n):
+            gl = tfr["logits"][i][slot].astype(np.float64)
+            o = lo[i].astype(np.float64)
+            rms = np.sqrt(np.mean(o * o))
+            worst = max(worst, float(np.max(np.abs(gl - o)) / rms))
+            worst_rms = max(worst_rms, float(np.sqrt(np.mean((gl - o) ** 2)) / rms))
+            if lo64 is not None:
+                floor = max(floor, float(np.max(np.abs(lo64[i].astype(np.float64) - o)) / rms))
+    print(f"[full] teacher-forced logits of rollouts {[(u, j) for (_, u, j) in chosen]}, steps 0-{LOGIT_STEPS - 1}: "
+          f"max|d|/rms {worst:.4f}, relative rms {worst_rms:.4f}, oracle fp32-vs-fp64 {floor:.4f}", flush=True)
+    assert worst_rms <= 3e-2
+    assert worst <= FULL_DEPTH_MAX_REL[name]
