@@ -38,11 +38,18 @@ TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_decode_qwen1p5b_sh
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2607_26253_amd", "csrc", "model_kernels.hip")
 
 
-def measured_traffic(kernel):
+# the workload and options the committed counter summary was taken on
+TRAFFIC_WORKLOAD = "qwen1p5b_shape"
+
+
+def measured_traffic(kernel, cfg, mode="sara", top_p=1.0):
     """HBM-side bytes per launch of `kernel` from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary (calibrated on a copy of known size), with
     the algorithmic bytes of the same launches; None when the summary does not
-    cover the kernel or the kernel source changed since it was taken."""
+    cover the kernel, was taken on another workload (the counters depend on
+    the weight shapes) or the kernel source changed since it was taken."""
+    if cfg["name"] != TRAFFIC_WORKLOAD or mode != "sara" or top_p != 1.0:
+        return None
     import hashlib
     try:
         text = open(TRAFFIC_PROFILE).read()
@@ -336,7 +343,7 @@ def main():
         # (peak flop/s over peak byte/s)
         ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
         mfma = cfg["model"]["dtype"] == "bf16" and per_launch_by > 0 and per_launch_fl / per_launch_by > ridge
-        tr = measured_traffic(dom["name"])
+        tr = measured_traffic(dom["name"], cfg, args.mode, args.top_p)
         out["roofline"] = {
             "kernel": dom["name"], "bound": "mfma" if mfma else "hbm",
             "achieved": ach_tfs if mfma else ach_gbs,
