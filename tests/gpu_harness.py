@@ -8,12 +8,19 @@ import workloads as W
 _WEIGHTS = {}
 
 
+_WEIGHT_CACHE_MODELS = 8
+
+
 def cached_weights(cfg):
-    """Weights of cfg's model, reused by consecutive tests of the same model
-    (a few GB at full vocabulary; the two most recent models are kept)."""
+    """Weights of cfg's model (its shape and master seed), generated once per
+    test session and shared by every test of that model: the four workloads'
+    full models and their 2-layer truncations hold about 26 GB of host
+    memory; beyond _WEIGHT_CACHE_MODELS models the least recently used goes."""
     key = (W.master_seed(cfg), tuple(sorted(cfg["model"].items())))
-    if key not in _WEIGHTS:
-        while len(_WEIGHTS) >= 2:
+    if key in _WEIGHTS:
+        _WEIGHTS[key] = _WEIGHTS.pop(key)          # most recently used last
+    else:
+        while len(_WEIGHTS) >= _WEIGHT_CACHE_MODELS:
             _WEIGHTS.pop(next(iter(_WEIGHTS)))
         _WEIGHTS[key] = W.make_weights(cfg)
     return _WEIGHTS[key]

@@ -128,7 +128,7 @@ def test_bf16_slice_full_depth(name):
     cfg = slice_cfg(name)
     print(f"[slice] {name}: L={cfg['model']['n_layers']} d={cfg['model']['d_model']} "
           f"alloc={ {k: cfg['alloc'][k] for k in ('B', 'budget_N', 'n_slots', 'pool_U', 'max_new')} }", flush=True)
-    w = W.make_weights(cfg)
+    w = cached_weights(cfg)
     pool = W.make_pool(cfg, 0)
     seed = W.sampling_seed(cfg)
     ora = ORUN.run_step(cfg, w, pool, seed, keep_logits=lambda u, j, i: True)
@@ -366,7 +366,7 @@ def test_logical_rollout_keys_give_exact_counterfactuals():
     cfg = W.parity_slice(W.get_config("qwen1p5b_shape"), B=8, N=96, max_new=10, pool_U=32)
     fk = W.fixed_k_variant(cfg)
     fk["alloc"]["budget_N"] = cfg["alloc"]["pool_U"] * cfg["alloc"]["k"]
-    w = W.make_weights(cfg)
+    w = cached_weights(cfg)
     pool = W.make_pool(cfg, 0)
     k = cfg["alloc"]["k"]
     ctx, _ = device_setup(cfg, w)

@@ -31,7 +31,7 @@ from oracle import grpo as OG
 from oracle import reward as OR
 from oracle import sampler as OS
 from oracle.model import Decoder
-from tests.gpu_harness import compare_logs, device_setup, forced_table, run_gpu_step
+from tests.gpu_harness import cached_weights, compare_logs, device_setup, forced_table, run_gpu_step
 from tests.test_gpu_bf16_slices import FULL_DEPTH_MAX_REL
 
 pytestmark = pytest.mark.gpu
@@ -52,7 +52,7 @@ def test_full_size_step(name, step):
     print(f"[full] {name} step {step}: {m['n_layers']} layers, {a['n_slots']} slots, max_new {a['max_new']}",
           flush=True)
     seed = W.sampling_seed(cfg)
-    ctx, w = device_setup(cfg)
+    ctx, w = device_setup(cfg, cached_weights(cfg))
     print("[full] running the GPU step (graph replay)", flush=True)
     gpu = run_gpu_step(ctx, cfg, pool, use_graph=True)
     # the same step again, eager and teacher forced with the GPU's own tokens,
