@@ -1346,24 +1346,33 @@ __device__ __forceinline__ void qkv_rope_mblock(const uint16_t* __restrict__ X, 
   __syncthreads();   // red is reused by the next m-block
 }
 
-// Live row count read on the device; m-blocks of up to 128 rows, each with
-// just enough 16-row activation tiles.  Grid: one block per weight tile.
+// Live row count read on the device.  Grid: x = one block per weight tile,
+// z = one block per 128 rows of the capacity.  The live 16-row activation
+// tiles are shared out in contiguous runs over the first min(gridDim.z,
+// zspread) z blocks (at most 8 tiles per block), so that a small batch keeps
+// several blocks per weight tile busy instead of one; zspread is chosen on
+// the host so that the whole grid's working blocks stay resident at once.
+// Every tile's arithmetic is the same whichever block computes it.
 // KS = d_model / 128, one of 4, 8, 12, 16, 24, 32 (checked by sara_init).
 template <int HD, int KS>
 __global__ __launch_bounds__(256) void k_qkv_rope(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
     const int32_t* __restrict__ M_ptr, int K, const RowDesc* __restrict__ rows,
     const float2* __restrict__ row_rope, int hq, int hkv, int layer, int64_t n_blocks,
-    uint16_t* __restrict__ qbuf, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
+    uint16_t* __restrict__ qbuf, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc, int zspread) {
   __shared__ f32x4 red[4][8][64];
   const int M = *M_ptr;
-  // one z block per 128-row m-block of the capacity (those past M exit)
-  for (int m_base = blockIdx.z * 128; m_base < M; m_base += gridDim.z * 128) {
-    const int mt = min(8, (M - m_base + 15) >> 4);
-    // depth: every k step (at most 16) in flight for up to 32 rows, then a half and a quarter
+  const int ntl = (M + 15) >> 4;
+  const int zs = max(1, min((int)gridDim.z, zspread));
+  const int tpz = min(8, (ntl + zs - 1) / zs);      // tiles per z block
+  for (int m_base = blockIdx.z * tpz * 16; m_base < M; m_base += gridDim.z * tpz * 16) {
+    const int mt = min(tpz, (M - m_base + 15) >> 4);
+    // depth: every k step (at most 12) in flight for up to 32 rows, then a
+    // half and a quarter (half of them from 16 k steps on, which keeps the
+    // register count low enough for two blocks per CU)
 #define SARA_QR(MT_, D_) \
     if (mt == MT_) qkv_rope_mblock<HD, MT_, D_, KS>(X, W, M, m_base, K, red, rows, row_rope, hq, hkv, layer, \
                                                     n_blocks, qbuf, kc, vc);
-    constexpr int D1 = KS <= 16 ? KS : KS / 2, D3 = D1 / 2, D5 = D1 / 4;
+    constexpr int D1 = KS < 16 ? KS : KS / 2, D3 = D1 / 2, D5 = D1 / 4;
     SARA_QR(1, D1) SARA_QR(2, D1) SARA_QR(3, D3) SARA_QR(4, D3)
     SARA_QR(5, D5) SARA_QR(6, D5) SARA_QR(7, D5) SARA_QR(8, D5)
 #undef SARA_QR
@@ -2131,6 +2140,22 @@ static void gemm_swiglu(sara_ctx* c, const void* X, const void* W, const int32_t
                        (const uint16_t*)W, (void*)c->xa, M_ptr, N, K, K, (int64_t)0, SampleArgs{});
 }
 
+// z blocks over which the q|k|v kernel shares out a small batch's 16-row
+// tiles: as many per weight tile as keep every working block resident at
+// once (blocks per CU x CUs / weight tiles), computed once per context
+template <typename F>
+static int qkv_spread(sara_ctx* c, F kernel) {
+  if (c->qkv_spread == 0) {
+    int per_cu = 0, dev = 0, n_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, 0) != hipSuccess ||
+        hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      per_cu = 1, n_cu = 256;
+    c->qkv_spread = std::max(1, std::max(1, per_cu) * std::max(1, n_cu) / std::max(1, c->nqkv / 16));
+  }
+  return c->qkv_spread;
+}
+
 // persistent attention grid: enough blocks for two per CU, never more than items
 static int attn_grid(sara_ctx* c, int M_cap) {
   int items = M_cap * c->hkv * c->attn_splits_max;
@@ -2182,7 +2207,8 @@ static void layers_T(sara_ctx* c, const int32_t* M_ptr, int M_cap, bool final_no
       launch_k(c, st, (k_qkv_rope<HD, KS_>), dim3(c->nqkv / 16, 1, (M_cap + 127) / 128), dim3(256), 0, \
                (const uint16_t*)x, \
                          (const uint16_t*)c->w_qkv[l], M_ptr, d, c->rows, c->row_rope, c->hq, c->hkv, l, \
-                         c->n_blocks, (uint16_t*)c->qbuf, (uint16_t*)c->kc, (uint16_t*)c->vc)
+                         c->n_blocks, (uint16_t*)c->qbuf, (uint16_t*)c->kc, (uint16_t*)c->vc, \
+                         qkv_spread(c, k_qkv_rope<HD, KS_>))
       switch (d / 128) {
         case 4: SARA_QKV(4); break;
         case 8: SARA_QKV(8); break;

@@ -119,6 +119,7 @@ struct sara_ctx {
   sara::AttnItem* attn_items = nullptr; // [S * dec_splits_max] decode attention work list of the step
   int32_t* attn_nitems = nullptr; // its length
   int attn_dec_grid = 0;          // blocks of the decode attention that are resident at once
+  int qkv_spread = 0;             // z blocks sharing a decode batch's tiles in the q|k|v kernel
 
   // prompt pool (library copies)
   int32_t* tok = nullptr;

@@ -311,6 +311,54 @@ def test_bf16_two_layer_full_length_contexts(name):
 # and every row's max|d| to P5_MAX_REL * rms, 1.5x the oracle's own spread
 # rounded up.
 P5_MAX_REL = 0.04
+def _logits_by_rollout(cfg, w, pool, slots):
+    """One free-running step of cfg on `slots` slots: every generated
+    position's logits keyed by (uid, j, index), the rollouts and the logs."""
+    import torch
+
+    from tests.gpu_harness import upload_pool
+    c = copy.deepcopy(cfg)
+    c["alloc"]["n_slots"] = slots
+    ctx, _ = device_setup(c, w)
+    d_tok, d_p, d_fl = upload_pool(pool)
+    ctx.sara_begin_step(d_tok, pool["offsets"], d_p, d_fl, pool["step"])
+    bufs = []
+    while not ctx.sara_query()["done"]:
+        buf = torch.zeros((slots, c["model"]["vocab"]), dtype=torch.float32, device="cuda")
+        ctx.sara_decode_step(None, buf, False)
+        bufs.append(buf)
+        ctx.sara_posterior_decide()
+        ctx.sara_refill()
+    ctx.sara_finish_step(1e-6)
+    logs, roll = ctx.read_logs(), ctx.read_rollouts()
+    ctx.close()
+    return {key: bufs[t][s] for (t, s), key in slot_rows(dict(logs=logs)).items()}, roll, logs
+
+
+def test_bf16_row_logits_independent_of_launch_grid():
+    """A row's logits depend on its own context only, not on the batch it
+    sits in or the launch grid: the same step on 40, 160 and 512 slots (one,
+    two and four z blocks per decode launch; the q|k|v kernel then shares the
+    batch's 16-row tiles out over several blocks, the last one ragged) gives
+    bit-identical logits at every generated position, and so the same
+    rollouts and decisions (1.5B shape, first 2 layers, full vocabulary)."""
+    import torch
+    cfg = W.parity_slice(W.get_config("qwen1p5b_shape"), B=4, N=40, max_new=6, pool_U=16)
+    cfg["model"]["n_layers"] = 2
+    w = cached_weights(cfg)
+    pool = W.make_pool(cfg, 0)
+    ref, rroll, rlogs = _logits_by_rollout(cfg, w, pool, 40)
+    assert len(ref) > 0
+    for slots in (160, 512):
+        got, roll, logs = _logits_by_rollout(cfg, w, pool, slots)
+        assert set(got) == set(ref)
+        bad = [key for key in ref if not torch.equal(got[key], ref[key])]
+        assert not bad, f"{len(bad)} of {len(ref)} rows differ on {slots} slots, e.g. {bad[:3]}"
+        assert np.array_equal(roll["tokens"], rroll["tokens"])
+        assert np.array_equal(logs["decisions"][:, :5], rlogs["decisions"][:, :5])
+        print(f"[grid] {slots} slots: {len(ref)} generated positions bit-identical to 40 slots", flush=True)
+
+
 P5_SLICES = {
     "qwen1p5b_shape": dict(steps=(0,)),
     "qwen3b_shape": dict(steps=(0,)),
