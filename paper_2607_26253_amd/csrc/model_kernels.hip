@@ -1366,9 +1366,9 @@ __global__ __launch_bounds__(256) void k_qkv_rope(const uint16_t* __restrict__ X
   const int tpz = min(8, (ntl + zs - 1) / zs);      // tiles per z block
   for (int m_base = blockIdx.z * tpz * 16; m_base < M; m_base += gridDim.z * tpz * 16) {
     const int mt = min(tpz, (M - m_base + 15) >> 4);
-    // depth: every k step (at most 12) in flight for up to 32 rows, then a
-    // half and a quarter (half of them from 16 k steps on, which keeps the
-    // register count low enough for two blocks per CU)
+    // depth for up to 32 rows: every k step in flight below 16 k steps, half
+    // of them from 16 on (the 16-step instance then fits two blocks per CU);
+    // a half and a quarter of that for more rows
 #define SARA_QR(MT_, D_) \
     if (mt == MT_) qkv_rope_mblock<HD, MT_, D_, KS>(X, W, M, m_base, K, red, rows, row_rope, hq, hkv, layer, \
                                                     n_blocks, qbuf, kc, vc);
