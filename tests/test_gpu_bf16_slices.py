@@ -335,15 +335,16 @@ def _logits_by_rollout(cfg, w, pool, slots):
     return {key: bufs[t][s] for (t, s), key in slot_rows(dict(logs=logs)).items()}, roll, logs
 
 
-def test_bf16_row_logits_independent_of_launch_grid():
+@pytest.mark.parametrize("name", ["qwen1p5b_shape", "qwen3b_shape"])
+def test_bf16_row_logits_independent_of_launch_grid(name):
     """A row's logits depend on its own context only, not on the batch it
     sits in or the launch grid: the same step on 40, 160 and 512 slots (one,
     two and four z blocks per decode launch; the q|k|v kernel then shares the
-    batch's 16-row tiles out over several blocks, the last one ragged) gives
-    bit-identical logits at every generated position, and so the same
-    rollouts and decisions (1.5B shape, first 2 layers, full vocabulary)."""
+    batch's 16-row tiles out over up to 4 (1.5B) or 3 (3B) blocks, the last
+    one ragged) gives bit-identical logits at every generated position, and
+    so the same rollouts and decisions (first 2 layers, full vocabulary)."""
     import torch
-    cfg = W.parity_slice(W.get_config("qwen1p5b_shape"), B=4, N=40, max_new=6, pool_U=16)
+    cfg = W.parity_slice(W.get_config(name), B=4, N=40, max_new=6, pool_U=16)
     cfg["model"]["n_layers"] = 2
     w = cached_weights(cfg)
     pool = W.make_pool(cfg, 0)
@@ -356,7 +357,8 @@ def test_bf16_row_logits_independent_of_launch_grid():
         assert not bad, f"{len(bad)} of {len(ref)} rows differ on {slots} slots, e.g. {bad[:3]}"
         assert np.array_equal(roll["tokens"], rroll["tokens"])
         assert np.array_equal(logs["decisions"][:, :5], rlogs["decisions"][:, :5])
-        print(f"[grid] {slots} slots: {len(ref)} generated positions bit-identical to 40 slots", flush=True)
+        print(f"[grid] {name}, {slots} slots: {len(ref)} generated positions bit-identical to 40 slots",
+              flush=True)
 
 
 P5_SLICES = {
